@@ -1,0 +1,123 @@
+"""Greedy acceptance oracle: per-row vocabulary argmax and the walk of Algorithm 1.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
+
+* ``argmax_rows``  -- t_v = argmax_w rows[v](w), the target-greedy token of every
+  verified row (Algorithm 1, App. B).  Ties go to the lowest index, as numpy's
+  argmax does (it returns the first maximum); a NaN counts as larger than every
+  number and the first NaN wins, again numpy's rule.  +0 and -0 compare equal.
+* ``greedy_walk``  -- Algorithm 1's loop: start at the root, take the argmax
+  token of the current row, descend to the child carrying that token if the
+  tree has one, otherwise stop and return the token as the new root.  The
+  child is looked up by a linear scan over the nodes in index order, so if a
+  (malformed) tree has two siblings with the same token the lower index wins.
+* ``accepted_length_def1`` -- an independent evaluation of Def. 1 (Sec. 3.3):
+  A(T) = max{k >= 0 : Y_{1:j} in T for all j <= k}.  For every node it climbs to
+  the root and checks that every edge carries the argmax token of the parent
+  row; the answer is the deepest such node.
+
+A round commits a + 1 tokens: the a accepted tree tokens and the bonus token
+read off the last verified row (Sec. 3.1, Eq. 1).
+"""
+
+import numpy as np
+
+
+def argmax_rows(logits):
+    """Row-wise argmax with lowest-index ties; logits [..., V] of any float dtype."""
+    if hasattr(logits, "detach"):
+        t = logits.detach().to("cpu")
+        if str(t.dtype) in ("torch.bfloat16", "torch.float16"):
+            t = t.float()
+        logits = t.numpy()
+    x = np.asarray(logits, dtype=np.float64)
+    return np.argmax(x, axis=-1).astype(np.int64)
+
+
+def _children_in_order(parents, v):
+    return [c for c in range(len(parents)) if parents[c] == v]
+
+
+def greedy_walk(argmax_row, parents, tokens):
+    """Algorithm 1's walk over one packed tree.
+
+    argmax_row [n]  target-greedy token of each node's row
+    parents    [n]  parents[0] = -1
+    tokens     [n]  tokens[0] = root b; tokens[c] is the token on the edge into c
+
+    Returns (a, path, next_root): a accepted non-root tokens, path = node ids
+    from the root to the last accepted node (length a + 1), and next_root =
+    argmax_row[path[-1]], the bonus token that becomes the next root.
+    """
+    parents = [int(p) for p in parents]
+    tokens = [int(t) for t in tokens]
+    argmax_row = [int(t) for t in argmax_row]
+    v = 0
+    path = [0]
+    for _ in range(len(parents)):
+        t = argmax_row[v]
+        nxt = None
+        for c in _children_in_order(parents, v):
+            if tokens[c] == t:
+                nxt = c
+                break
+        if nxt is None:
+            return len(path) - 1, path, t
+        path.append(nxt)
+        v = nxt
+    raise ValueError("walk did not terminate: parents do not form a tree")
+
+
+def accepted_length_def1(argmax_row, parents, tokens):
+    """Def. 1 evaluated directly: the deepest node whose whole root path is target-greedy.
+
+    Returns (a, path) where path is that node's chain from the root (the root
+    alone when no child of the root matches).
+    """
+    parents = [int(p) for p in parents]
+    tokens = [int(t) for t in tokens]
+    argmax_row = [int(t) for t in argmax_row]
+    best_depth, best_node = 0, 0
+    for c in range(len(parents)):
+        chain = [c]
+        while parents[chain[-1]] >= 0:
+            chain.append(parents[chain[-1]])
+        chain.reverse()  # root ... c
+        ok = all(tokens[chain[k + 1]] == argmax_row[chain[k]] for k in range(len(chain) - 1))
+        depth = len(chain) - 1
+        if ok and depth > best_depth:
+            best_depth, best_node = depth, c
+    path = [best_node]
+    while parents[path[-1]] >= 0:
+        path.append(parents[path[-1]])
+    path.reverse()
+    return best_depth, path
+
+
+def greedy_accept(logits, parents, tokens, path_stride=None):
+    """Batched acceptance: argmax of every row, then the walk of every sequence.
+
+    logits [batch][n][V]; parents, tokens [batch][n].
+    Returns dict with argmax [batch][n], accept_len [batch], accept_path
+    [batch][path_stride] (-1 padded), next_root [batch], committed (list of the
+    a + 1 committed tokens per sequence).
+    """
+    am = argmax_rows(logits)
+    parents = np.asarray(parents if not hasattr(parents, "numpy") else parents.cpu().numpy())
+    tokens = np.asarray(tokens if not hasattr(tokens, "numpy") else tokens.cpu().numpy())
+    batch, n = am.shape
+    if path_stride is None:
+        path_stride = n
+    acc = np.zeros(batch, dtype=np.int64)
+    paths = -np.ones((batch, path_stride), dtype=np.int64)
+    roots = np.zeros(batch, dtype=np.int64)
+    committed = []
+    for b in range(batch):
+        a, path, nr = greedy_walk(am[b], parents[b], tokens[b])
+        acc[b] = a
+        k = min(len(path), path_stride)
+        paths[b, :k] = path[:k]
+        roots[b] = nr
+        committed.append([int(tokens[b][c]) for c in path[1:]] + [int(nr)])
+    return {"argmax": am, "accept_len": acc, "accept_path": paths, "next_root": roots,
+            "committed": committed}
