@@ -1,0 +1,299 @@
+"""Benchmark of one GLANCE decode round on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+block-draft attention, then tree-verify attention, then greedy acceptance
+(vocabulary argmax of every verified row and the walk), back to back on one
+stream.  The workload is the grounded long-document configuration: batch 4,
+28 query / 4 KV heads, head_dim 128, bf16, 16384 context tokens per sequence
+(14336 image + 2048 text), a 16-row draft block and a 64-row tree, verified
+rows over a 152064-token vocabulary.
+
+Inputs are resident in HBM before timing starts.  Several copies of the input
+set rotate from step to step so that each step's context reads miss the
+256 MB last-level cache (a step reads about 350 MB).  The draft and the
+verify read separate caches (the draft head's and the target's).
+
+Prints one JSON line: whole-round latency (value, from the wall clock over the
+timed steps), achieved KV HBM bandwidth, a per-kernel breakdown from HIP
+events recorded on the library's stream, the roofline of the dominant kernel
+and the float64 oracle timed on the host cores.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="doc_16k")
+    ap.add_argument("--sets", type=int, default=4, help="input copies rotated across steps")
+    ap.add_argument("--graph", action="store_true", help="replay the round from a captured HIP graph")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle timing")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def kv_bytes(w, ctx_lens):
+    return int(sum(int(c) for c in ctx_lens)) * w.hkv * w.d * 2 * 2  # K and V, bf16
+
+
+def attn_flops(w, ctx_lens, n, visible_new):
+    """4*D flops (Q.K and P.V) per (query head, row, visible key)."""
+    ctx_rows = sum(int(c) for c in ctx_lens) * n
+    return 4.0 * w.d * w.hq * (ctx_rows + visible_new)
+
+
+def tree_visible_pairs(parents):
+    """sum over nodes of |ancestors-or-self| (the visible tree keys of the verify)."""
+    tot = 0
+    for par in parents:
+        par = [int(x) for x in par]
+        for i in range(len(par)):
+            j = i
+            while j >= 0:
+                tot += 1
+                j = par[j]
+    return tot
+
+
+def source_hash(path):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def load_traffic(kernel_key, src):
+    """HBM bytes per launch measured with rocprofv3 counters, if taken on the current source."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        rec = json.load(open(p)).get(kernel_key)
+    except Exception:
+        return None
+    if not rec or rec.get("source_sha") != source_hash(src):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(inputs, budget_s):
+    """The float64 oracle, as it stands, on a bounded sample of the same round."""
+    import numpy as np
+    from oracle import accept as OA
+    from oracle import attention as OT
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    w = inputs["workload"]
+    d, v = inputs["draft"], inputs["verify"]
+    rows_per_batch = []
+    t0 = time.perf_counter()
+    done_b = 0
+    # one sequence of the batch at a time (draft + verify + accept of that sequence)
+    for b in range(w.batch):
+        sl = slice(b, b + 1)
+        OT.block_draft_attn(d["q"][sl], d["k_ctx"][sl], d["v_ctx"][sl], d["k_new"][sl], d["v_new"][sl],
+                            d["ctx_lens"][sl])
+        OT.tree_verify_attn(v["q"][sl], v["k_ctx"][sl], v["v_ctx"][sl], v["k_new"][sl], v["v_new"][sl],
+                            v["ctx_lens"][sl], inputs["parents"][sl])
+        OA.greedy_accept(inputs["logits"][sl], inputs["parents"][sl], inputs["tokens"][sl])
+        done_b += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    per_round_us = dt / done_b * w.batch * 1e6
+    rows_per_batch.append(done_b)
+    return {"value": round(per_round_us, 1), "unit": "us per round", "cores": int(cores), "kind": "oracle",
+            "sample": f"{done_b} of {w.batch} sequences of one {w.name} round (draft + verify + accept, "
+                      f"numpy float64), scaled to the full round; {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE={world}). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_00355_amd as G
+    from workloads import configs as C
+
+    if not os.path.exists(G.LIB_PATH):
+        from paper_2609_00355_amd import build
+        build.build()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+
+    w = C.WORKLOADS[args.workload]
+    t_gen = time.perf_counter()
+    inputs = C.round_inputs(w, seed=0)
+    t_gen = time.perf_counter() - t_gen
+    ctx = inputs["ctx_lens"]
+    stream = torch.cuda.current_stream()
+
+    # ---- device copies of the input set, outputs and prepared calls
+    sets = []
+    for r in range(args.sets):
+        dd = {k: t.to(dev) for k, t in inputs["draft"].items()}
+        vv = {k: t.to(dev) for k, t in inputs["verify"].items()}
+        par = inputs["parents"].to(dev)
+        tok = inputs["tokens"].to(dev)
+        logits = inputs["logits"].to(dev)
+        d_call, d_out, _ = G.prepare_block_draft_attn(dd["q"], dd["k_ctx"], dd["v_ctx"], dd["k_new"],
+                                                      dd["v_new"], dd["ctx_lens"])
+        v_call, v_out, _ = G.prepare_tree_verify_attn(vv["q"], vv["k_ctx"], vv["v_ctx"], vv["k_new"],
+                                                      vv["v_new"], vv["ctx_lens"], par)
+        a_call, a_out = G.prepare_greedy_accept(logits, par, tok, path_stride=16)
+        sets.append({"draft": d_call, "verify": v_call, "accept": a_call, "a_out": a_out,
+                     "keep": (dd, vv, par, tok, logits, d_out, v_out)})
+    torch.cuda.synchronize()
+
+    def step(s):
+        s["draft"]()
+        s["verify"]()
+        s["accept"]()
+
+    graphs = None
+    if args.graph:
+        graphs = []
+        for s in sets:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(s)
+            graphs.append(g)
+        torch.cuda.synchronize()
+
+    for i in range(args.warmup):
+        if graphs:
+            graphs[i % len(graphs)].replay()
+        else:
+            step(sets[i % len(sets)])
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly K steps, synchronised on both sides
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        if graphs:
+            graphs[i % len(graphs)].replay()
+        else:
+            step(sets[i % len(sets)])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    us_round = wall / args.steps * 1e6
+
+    # ---- per-kernel durations: HIP events recorded by the library around each
+    # call's main kernel, on the same stream, over the same number of steps
+    names = ("draft", "verify", "accept")
+    evs = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)] for k in names}
+    rounds = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    for pairs in list(evs.values()) + [rounds]:  # torch creates the HIP events lazily, at first record
+        for a, b in pairs:
+            a.record(stream)
+            b.record(stream)
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        s = sets[i % len(sets)]
+        rounds[i][0].record(stream)
+        for k in names:
+            G.glance_set_kernel_events(*evs[k][i])
+            s[k]()
+        rounds[i][1].record(stream)
+    torch.cuda.synchronize()
+    k_us = {k: float(np.mean([a.elapsed_time(b) for a, b in evs[k]]) * 1e3) for k in names}
+    round_gpu_us = float(np.mean([a.elapsed_time(b) for a, b in rounds]) * 1e3)
+
+    # ---- algorithmic work per launch
+    kvb = kv_bytes(w, ctx)
+    qo_draft = w.batch * w.n_draft * w.hq * w.d * 2 * 2 + w.batch * w.n_draft * w.hkv * w.d * 2 * 2
+    qo_verify = w.batch * w.n_tree * w.hq * w.d * 2 * 2 + w.batch * w.n_tree * w.hkv * w.d * 2 * 2
+    vis_tree = tree_visible_pairs(inputs["parents"].numpy())
+    f_draft = attn_flops(w, ctx, w.n_draft, w.batch * w.n_draft * w.n_draft)
+    f_verify = attn_flops(w, ctx, w.n_tree, vis_tree)
+    logit_bytes = w.batch * w.n_tree * w.vocab * 2
+    per_kernel = {
+        "draft": {"us": round(k_us["draft"], 2), "kernel": "attn_bf16_partial<128,false>",
+                  "gbps": round((kvb + qo_draft) / k_us["draft"] / 1e3, 1),
+                  "tflops": round(f_draft / k_us["draft"] / 1e6, 1)},
+        "verify": {"us": round(k_us["verify"], 2), "kernel": "attn_bf16_partial<128,true>",
+                   "gbps": round((kvb + qo_verify) / k_us["verify"] / 1e3, 1),
+                   "tflops": round(f_verify / k_us["verify"] / 1e6, 1)},
+        "accept": {"us": round(k_us["accept"], 2), "kernel": "argmax_partial<true,true>",
+                   "gbps": round(logit_bytes / k_us["accept"] / 1e3, 1)},
+    }
+    for k, bound in (("draft", "hbm"), ("verify", "mfma"), ("accept", "hbm")):
+        pk = per_kernel[k]
+        pk["bound"] = bound
+        pk["frac"] = round(pk["gbps"] / HBM_PEAK_GBS if bound == "hbm" else pk["tflops"] / MFMA_BF16_PEAK_TFLOPS, 3)
+
+    dom = max(names, key=lambda k: k_us[k])
+    src = os.path.join(ROOT, "paper_2609_00355_amd", "csrc",
+                       "accept.hip" if dom == "accept" else "attn_bf16.hip")
+    if dom == "verify":
+        roof = {"bound": "mfma", "achieved": round(f_verify / k_us["verify"] / 1e6, 1),
+                "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    elif dom == "draft":
+        roof = {"bound": "hbm", "achieved": round((kvb + qo_draft) / k_us["draft"] / 1e3, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(logit_bytes / k_us["accept"] / 1e3, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = load_traffic(dom, src)
+    roof["kernel"] = per_kernel[dom]["kernel"]
+
+    acc = sets[0]["a_out"]["accept_len"].cpu().numpy()
+    res = {
+        "metric": "draft+verify round latency (us) and achieved KV HBM GB/s at 16k ctx, 1 MI355X",
+        "value": round(us_round, 2),
+        "unit": "us per round",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: batch {w.batch}, {w.hq}/{w.hkv} heads, head_dim {w.d}, bf16, "
+                               f"ctx {w.ctx} ({w.image} image + {w.ctx - w.image} text) per sequence, "
+                               f"draft block {w.n_draft}, tree {w.n_tree} rows, vocab {w.vocab}",
+                   "global_batch": w.batch, "seq_len": w.ctx, "parallelism": "single GPU",
+                   "launch": "graph replay" if graphs else "eager (prepared C-ABI calls)",
+                   "input_sets_rotated": args.sets},
+        "achieved_kv_gbps": round(2 * kvb / (k_us["draft"] + k_us["verify"]) / 1e3, 1),
+        "round_kv_gbps": round(2 * kvb / us_round / 1e3, 1),
+        "round_gpu_us_events": round(round_gpu_us, 2),
+        "kernels": per_kernel,
+        "roofline": roof,
+        "synthetic_tau": round(1.0 + float(acc.mean()), 3),
+        "input_gen_s": round(t_gen, 1),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(inputs, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,205 @@
+/*
+ * glance.h -- C ABI of the GLANCE decode-round hot path on MI355X (gfx950).
+ *
+ * One GLANCE round (arXiv 2609.00355, Algorithm 1, App. B) runs two forward
+ * passes and a walk.  This library provides the data-parallel core of each:
+ *
+ *   glance_block_draft_attn  attention of the one-pass block draft (Sec. 3.2):
+ *                            the block (pending root b + B-1 mask tokens) attends
+ *                            to the whole cached multimodal context and,
+ *                            bidirectionally, to itself;
+ *   glance_tree_verify_attn  attention of the one-pass tree verification
+ *                            (Def. 1, Sec. 3.3): root b and the candidate tree
+ *                            are packed behind an ancestor mask, so node i sees
+ *                            the context plus exactly its ancestors and itself;
+ *   glance_greedy_accept     the target-greedy token of every verified row
+ *                            (vocabulary argmax, lowest index on ties) and the
+ *                            walk of Algorithm 1: the longest root-to-node path
+ *                            whose every edge carries the parent row's argmax,
+ *                            plus the bonus token that becomes the next root.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Data pointers marked "device" are HIP device pointers owned by the caller.
+ *    The library never allocates, frees or copies to the host on these paths;
+ *    all scratch memory is the caller's `workspace`, sized by the matching
+ *    *_workspace_size() call.  Inputs are never written.
+ *  - Work is enqueued on `stream` (0 = the null stream) and the call returns
+ *    without synchronising.  Calls on different streams must use different
+ *    workspaces; calls that share a workspace must be ordered on one stream.
+ *  - The return status covers everything checkable on the host: null or
+ *    misaligned (16-byte) pointers, unsupported shapes and a workspace that is
+ *    too small.  These checks run before any HIP call.  A failed kernel launch
+ *    returns GLANCE_ERR_HIP.  glance_last_error() gives the detail of the
+ *    calling thread's last non-OK status.
+ *  - Device integer inputs (ctx_lens, parents, tokens) are not checked on the
+ *    hot path (that would need a device-to-host copy).  They are made safe to
+ *    read: each ctx_len is clamped to [0, ctx_capacity], and a parent index
+ *    that is not in [0, node) ends that node's ancestor chain.  Use
+ *    glance_validate_tree() on host copies to reject malformed trees.
+ *  - All arithmetic accumulates in fp32.  Q, K, V and O share one dtype.
+ */
+#ifndef GLANCE_H
+#define GLANCE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GLANCE_OK = 0,
+  GLANCE_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad size or shape */
+  GLANCE_ERR_UNSUPPORTED = -2, /* well-formed but outside this build's limits */
+  GLANCE_ERR_WORKSPACE = -3,   /* workspace null or smaller than required */
+  GLANCE_ERR_HIP = -4          /* a HIP call failed; see glance_last_error() */
+} glance_status;
+
+typedef enum { GLANCE_F32 = 0, GLANCE_BF16 = 1 } glance_dtype;
+
+/*
+ * Shape of one attention call.
+ *   batch         sequences in the call, >= 1
+ *   n_new         new rows per sequence: the block size B (draft) or the tree
+ *                 rows including the root (verify); 1..64 (one 64-bit ancestor
+ *                 word per node; the paper's trees have 63 nodes + root, Sec. 3.3)
+ *   n_q_heads     query heads Hq; n_q_heads % n_kv_heads == 0 and
+ *                 n_q_heads / n_kv_heads <= 16.  Query head h reads KV head
+ *                 h / (Hq/Hkv) (contiguous grouped-query attention).
+ *   n_kv_heads    KV heads Hkv, >= 1
+ *   head_dim      D, 64 or 128
+ *   ctx_capacity  token stride of the context cache (>= every ctx_len), >= 0
+ *   sm_scale      softmax scale; <= 0 selects 1/sqrt(head_dim)
+ *   dtype         dtype of Q, K, V and O
+ *   split_keys    context keys per split-KV work item; 0 lets the library
+ *                 choose.  Otherwise a multiple of 64.  Results agree with any
+ *                 other choice within rounding.
+ */
+typedef struct {
+  int32_t batch;
+  int32_t n_new;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t ctx_capacity;
+  float sm_scale;
+  glance_dtype dtype;
+  int32_t split_keys;
+} glance_attn_shape;
+
+/*
+ * Block-draft attention (Sec. 3.2).  For every sequence b, query head h and
+ * block row i:
+ *     keys = [K_ctx[b, g, 0:ctx_b] ; K_new[b, 0:n_new, g]],   g = h / (Hq/Hkv)
+ *     out[b,i,h] = softmax(sm_scale * q[b,i,h] . keys^T) . values
+ * with every key visible to every row (the block is bidirectional and sees
+ * the whole context).  Row 0 is the pending root b, rows 1.. are mask tokens;
+ * the kernel is position-agnostic (Q and K are post-rotary).
+ *
+ *   q         device [batch][n_new][Hq][D]              dtype
+ *   k_ctx     device [batch][Hkv][ctx_capacity][D]      dtype (may be NULL iff ctx_capacity == 0)
+ *   v_ctx     device [batch][Hkv][ctx_capacity][D]      dtype (idem)
+ *   k_new     device [batch][n_new][Hkv][D]             dtype, keys of the block rows
+ *   v_new     device [batch][n_new][Hkv][D]             dtype
+ *   ctx_lens  device [batch] int32, context tokens per sequence (root excluded)
+ *   out       device [batch][n_new][Hq][D]              dtype
+ *   lse       device [batch][n_new][Hq] float32 natural-log sum-exp of the
+ *             scaled scores, or NULL
+ *   workspace device, >= glance_attn_workspace_size(s) bytes, 256-byte aligned
+ */
+glance_status glance_block_draft_attn(const glance_attn_shape* s, const void* q, const void* k_ctx,
+                                      const void* v_ctx, const void* k_new, const void* v_new,
+                                      const int32_t* ctx_lens, void* out, float* lse,
+                                      void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Tree-verify attention (Def. 1, Sec. 3.3; "pack b and T with an ancestor
+ * mask", Algorithm 1).  Same as the draft except for the new keys: row i sees
+ * new key j iff j == i or j is an ancestor of i in the tree given by
+ *   parents   device [batch][n_new] int32; parents[b][0] = -1 (row 0 is the
+ *             root b) and 0 <= parents[b][i] < i for i >= 1.
+ * The row of a depth-d node then carries the target's conditioning on
+ * x o b o y_{1:d}.  Positions (ctx_b + depth) are the caller's business:
+ * Q and K arrive post-rotary.
+ */
+glance_status glance_tree_verify_attn(const glance_attn_shape* s, const void* q, const void* k_ctx,
+                                      const void* v_ctx, const void* k_new, const void* v_new,
+                                      const int32_t* ctx_lens, const int32_t* parents, void* out,
+                                      float* lse, void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
+
+/*
+ * Greedy acceptance (Algorithm 1's loop; Def. 1's accepted length A(T)).
+ *   logits      device [batch][n_nodes][vocab], dtype logits_dtype (F32 or BF16);
+ *               row v is the verified distribution of node v, row 0 the root's
+ *   parents     device [batch][n_nodes] int32 (as for tree verify)
+ *   tokens      device [batch][n_nodes] int32; tokens[b][0] = root b,
+ *               tokens[b][c] = token on the edge into node c
+ *   argmax_out  device [batch][n_nodes] int32: argmax of each row.  Ties go to
+ *               the lowest index; +0 and -0 are equal; a NaN counts as larger
+ *               than every number and the first NaN wins.
+ *   accept_len  device [batch] int32: a, the number of accepted tree tokens
+ *   accept_path device [batch][path_stride] int32: node ids from the root to
+ *               the last accepted node (a + 1 entries), then -1.  Entries past
+ *               path_stride are dropped (accept_len still counts them);
+ *               path_stride >= 16 holds any tree of depth <= 15.
+ *   next_root   device [batch] int32: the bonus token argmax_out[b][last node],
+ *               which the round commits after the a accepted tokens and which
+ *               becomes the next round's root.
+ * Walk: v = 0; t = argmax(row v); if some child c of v has tokens[c] == t
+ * (lowest such c if siblings repeat a token), append c and continue from c,
+ * else stop.  Each step moves to a larger node index, so the walk ends within
+ * n_nodes steps even for malformed device data.
+ *   1 <= n_nodes <= 64, 1 <= vocab <= 2^30, path_stride >= 1.
+ */
+glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                   glance_dtype logits_dtype, const void* logits,
+                                   const int32_t* parents, const int32_t* tokens,
+                                   int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
+                                   int32_t path_stride, int32_t* next_root, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes an attention call with shape *s needs (0 if *s is invalid).
+ * The same size serves the draft and the verify entry point. Host only. */
+size_t glance_attn_workspace_size(const glance_attn_shape* s);
+
+/* Workspace bytes glance_greedy_accept needs (0 if the sizes are invalid). Host only. */
+size_t glance_accept_workspace_size(int32_t batch, int32_t n_nodes, int32_t vocab);
+
+/*
+ * Host-side check of one candidate tree (Def. 1): parents[0] == -1,
+ * 0 <= parents[i] < i, depth <= max_depth (max_depth < 0: no limit) and, when
+ * tokens_host is not NULL, distinct tokens among siblings (the tree is a set
+ * of strings).  Returns GLANCE_OK or GLANCE_ERR_INVALID_ARG with the reason in
+ * glance_last_error().  Host pointers; no GPU needed.
+ */
+glance_status glance_validate_tree(int32_t n, const int32_t* parents_host, const int32_t* tokens_host,
+                                   int32_t max_depth);
+
+/* Static description of a status code. */
+const char* glance_status_string(glance_status status);
+
+/* Detail of the calling thread's last non-OK status ("" if none). */
+const char* glance_last_error(void);
+
+/*
+ * Profiling hook.  When both events are non-NULL, the next attention or
+ * accept call on this thread records `start` on its stream right before its
+ * main kernel (the split-KV attention kernel, or the vocabulary argmax
+ * kernel) and `stop` right after it, then forgets the pair.  Arguments are
+ * hipEvent_t handles created by the caller.  Pass NULLs to clear.
+ */
+glance_status glance_set_kernel_events(void* start_event, void* stop_event);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int32_t glance_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GLANCE_H */

@@ -1,0 +1,344 @@
+"""Python binding of libglance.so, the GLANCE decode-round hot path on MI355X.
+
+Thin ctypes marshalling over the C ABI declared in include/glance.h: each
+function takes torch tensors that already live on the GPU, checks their
+dtype, layout and shape, and passes raw device pointers plus the current HIP
+stream to the library.  Outputs and workspaces the caller does not supply are
+allocated with torch (device memory plumbing); every step of the computation
+runs in the library's HIP kernels.  There is no fallback: if the library is
+missing or a GPU is absent, the calls raise.
+
+    glance_block_draft_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens) -> (out, lse)
+    glance_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents) -> (out, lse)
+    glance_greedy_accept(logits, parents, tokens) -> dict(argmax, accept_len, accept_path, next_root)
+
+Layouts: q, out [batch][n][Hq][D]; k_ctx, v_ctx [batch][Hkv][capacity][D];
+k_new, v_new [batch][n][Hkv][D]; ctx_lens [batch] int32; parents, tokens
+[batch][n] int32; logits [batch][n][vocab].
+"""
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libglance.so")
+
+GLANCE_OK, GLANCE_ERR_INVALID_ARG, GLANCE_ERR_UNSUPPORTED, GLANCE_ERR_WORKSPACE, GLANCE_ERR_HIP = \
+    0, -1, -2, -3, -4
+GLANCE_F32, GLANCE_BF16 = 0, 1
+
+
+class GlanceError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__(f"{detail} (status {status})")
+        self.status = status
+
+
+class AttnShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_new", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("ctx_capacity", ctypes.c_int32), ("sm_scale", ctypes.c_float),
+                ("dtype", ctypes.c_int), ("split_keys", ctypes.c_int32)]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_SZ = ctypes.c_size_t
+
+_SIGS = {
+    "glance_block_draft_attn": (ctypes.c_int, [ctypes.POINTER(AttnShape), _P, _P, _P, _P, _P, _P, _P, _P,
+                                               _P, _SZ, _P]),
+    "glance_tree_verify_attn": (ctypes.c_int, [ctypes.POINTER(AttnShape), _P, _P, _P, _P, _P, _P, _P, _P,
+                                               _P, _P, _SZ, _P]),
+    "glance_greedy_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P, _P, _I32,
+                                            _P, _P, _SZ, _P]),
+    "glance_attn_workspace_size": (_SZ, [ctypes.POINTER(AttnShape)]),
+    "glance_accept_workspace_size": (_SZ, [_I32, _I32, _I32]),
+    "glance_validate_tree": (ctypes.c_int, [_I32, _P, _P, _I32]),
+    "glance_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "glance_last_error": (ctypes.c_char_p, []),
+    "glance_set_kernel_events": (ctypes.c_int, [_P, _P]),
+    "glance_version": (_I32, []),
+}
+
+
+def lib():
+    """Load libglance.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_00355_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def _check(status):
+    if status != GLANCE_OK:
+        raise GlanceError(status, lib().glance_last_error().decode())
+
+
+def glance_status_string(status):
+    return lib().glance_status_string(int(status)).decode()
+
+
+def glance_last_error():
+    return lib().glance_last_error().decode()
+
+
+def glance_version():
+    return int(lib().glance_version())
+
+
+def glance_validate_tree(parents, tokens=None, max_depth=-1):
+    """Host check of one tree (Def. 1).  Returns (ok, message)."""
+    import numpy as np
+    par = np.ascontiguousarray(np.asarray(parents, dtype=np.int32))
+    tok = None if tokens is None else np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
+    st = lib().glance_validate_tree(int(par.size), par.ctypes.data,
+                                    None if tok is None else tok.ctypes.data, int(max_depth))
+    return st == GLANCE_OK, ("" if st == GLANCE_OK else glance_last_error())
+
+
+def attn_shape(batch, n_new, n_q_heads, n_kv_heads, head_dim, ctx_capacity, dtype, sm_scale=0.0,
+               split_keys=0):
+    return AttnShape(int(batch), int(n_new), int(n_q_heads), int(n_kv_heads), int(head_dim),
+                     int(ctx_capacity), float(sm_scale), int(dtype), int(split_keys))
+
+
+def glance_attn_workspace_size(shape):
+    return int(lib().glance_attn_workspace_size(ctypes.byref(shape)))
+
+
+def glance_accept_workspace_size(batch, n_nodes, vocab):
+    return int(lib().glance_accept_workspace_size(int(batch), int(n_nodes), int(vocab)))
+
+
+def glance_set_kernel_events(start, stop):
+    """Record torch.cuda.Event pair around the next call's main kernel (None, None clears)."""
+    a = None if start is None else ctypes.c_void_p(start.cuda_event)
+    b = None if stop is None else ctypes.c_void_p(stop.cuda_event)
+    _check(lib().glance_set_kernel_events(a, b))
+
+
+# ---------------------------------------------------------------- tensor helpers
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return GLANCE_F32
+    if t.dtype == torch.bfloat16:
+        return GLANCE_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}: use float32 or bfloat16")
+
+
+def _dev(t, name, dtype=None, ndim=None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
+    return t
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _workspace(nbytes, device, workspace):
+    torch = _torch()
+    if workspace is not None:
+        return workspace
+    # 256-byte aligned by the caching allocator
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def _attn(tree, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, workspace, sm_scale,
+          split_keys, stream, want_lse):
+    torch = _torch()
+    _dev(q, "q", ndim=4)
+    dt = q.dtype
+    code = _dtype_code(q)
+    batch, n, hq, d = q.shape
+    _dev(k_new, "k_new", dt, 4)
+    _dev(v_new, "v_new", dt, 4)
+    hkv = k_new.shape[2]
+    if tuple(k_new.shape) != (batch, n, hkv, d) or tuple(v_new.shape) != (batch, n, hkv, d):
+        raise ValueError("k_new / v_new must be [batch][n][Hkv][D] matching q")
+    if k_ctx is not None and k_ctx.numel() > 0:
+        _dev(k_ctx, "k_ctx", dt, 4)
+        _dev(v_ctx, "v_ctx", dt, 4)
+        cap = k_ctx.shape[2]
+        if tuple(k_ctx.shape) != (batch, hkv, cap, d) or tuple(v_ctx.shape) != (batch, hkv, cap, d):
+            raise ValueError("k_ctx / v_ctx must be [batch][Hkv][capacity][D]")
+    else:
+        cap, k_ctx, v_ctx = 0, None, None
+    _dev(ctx_lens, "ctx_lens", torch.int32, 1)
+    if ctx_lens.shape[0] != batch:
+        raise ValueError("ctx_lens must have one entry per sequence")
+    if tree:
+        _dev(parents, "parents", torch.int32, 2)
+        if tuple(parents.shape) != (batch, n):
+            raise ValueError("parents must be [batch][n]")
+    shape = attn_shape(batch, n, hq, hkv, d, cap, code, sm_scale, split_keys)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _dev(out, "out", dt, 4)
+    if lse is None and want_lse:
+        lse = torch.empty((batch, n, hq), dtype=torch.float32, device=q.device)
+    elif lse is not None:
+        _dev(lse, "lse", torch.float32, 3)
+    need = glance_attn_workspace_size(shape)
+    if need == 0:
+        raise GlanceError(GLANCE_ERR_INVALID_ARG, glance_last_error())
+    ws = _workspace(need, q.device, workspace)
+    common = [ctypes.byref(shape), _ptr(q), _ptr(k_ctx), _ptr(v_ctx), _ptr(k_new), _ptr(v_new),
+              _ptr(ctx_lens)]
+    if tree:
+        st = lib().glance_tree_verify_attn(*common, _ptr(parents), _ptr(out), _ptr(lse), _ptr(ws),
+                                           ws.numel() * ws.element_size(), _stream(stream))
+    else:
+        st = lib().glance_block_draft_attn(*common, _ptr(out), _ptr(lse), _ptr(ws),
+                                           ws.numel() * ws.element_size(), _stream(stream))
+    _check(st)
+    return out, lse
+
+
+def glance_block_draft_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, out=None, lse=None, workspace=None,
+                            sm_scale=0.0, split_keys=0, stream=None, want_lse=True):
+    """Block-draft attention (bidirectional block over the cached context).  Returns (out, lse)."""
+    return _attn(False, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, None, out, lse, workspace, sm_scale,
+                 split_keys, stream, want_lse)
+
+
+def glance_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out=None, lse=None,
+                            workspace=None, sm_scale=0.0, split_keys=0, stream=None, want_lse=True):
+    """Ancestor-masked tree-verify attention.  Returns (out, lse)."""
+    return _attn(True, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, workspace, sm_scale,
+                 split_keys, stream, want_lse)
+
+
+def glance_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None, workspace=None,
+                         stream=None):
+    """Row argmax + the walk of Algorithm 1.  Returns a dict of int32 GPU tensors."""
+    torch = _torch()
+    _dev(logits, "logits", ndim=3)
+    code = _dtype_code(logits)
+    batch, n, vocab = logits.shape
+    _dev(parents, "parents", torch.int32, 2)
+    _dev(tokens, "tokens", torch.int32, 2)
+    if tuple(parents.shape) != (batch, n) or tuple(tokens.shape) != (batch, n):
+        raise ValueError("parents / tokens must be [batch][n_nodes]")
+    path_stride = int(path_stride or n)
+    dev = logits.device
+    if outputs is None:
+        outputs = {
+            "argmax": torch.empty((batch, n), dtype=torch.int32, device=dev),
+            "accept_len": torch.empty((batch,), dtype=torch.int32, device=dev),
+            "accept_path": torch.empty((batch, path_stride), dtype=torch.int32, device=dev),
+            "next_root": torch.empty((batch,), dtype=torch.int32, device=dev),
+        }
+    need = glance_accept_workspace_size(batch, n, vocab)
+    if need == 0:
+        raise GlanceError(GLANCE_ERR_INVALID_ARG, glance_last_error())
+    ws = _workspace(need, dev, workspace)
+    st = lib().glance_greedy_accept(batch, n, vocab, code, _ptr(logits), _ptr(parents), _ptr(tokens),
+                                    _ptr(outputs["argmax"]), _ptr(outputs["accept_len"]),
+                                    _ptr(outputs["accept_path"]), path_stride,
+                                    _ptr(outputs["next_root"]), _ptr(ws),
+                                    ws.numel() * ws.element_size(), _stream(stream))
+    _check(st)
+    return outputs
+
+
+# ---------------------------------------------------------------- prepared calls
+class PreparedCall:
+    """A library call with all arguments checked and marshalled once.
+
+    Calling it re-issues the same C call (same pointers, same stream) with no
+    per-call Python argument processing, for launch loops and graph capture.
+    The tensors it references are kept alive by the object.
+    """
+
+    def __init__(self, fn, args, keep):
+        self._fn = fn
+        self._args = args
+        self._keep = keep
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != GLANCE_OK:
+            raise GlanceError(st, glance_last_error())
+
+
+def _prepare_attn(tree, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, workspace, sm_scale,
+                  split_keys, stream):
+    batch, n, hq, d = q.shape
+    hkv = k_new.shape[2]
+    cap = 0 if (k_ctx is None or k_ctx.numel() == 0) else k_ctx.shape[2]
+    shape = attn_shape(batch, n, hq, hkv, d, cap, _dtype_code(q), sm_scale, split_keys)
+    ws = _workspace(glance_attn_workspace_size(shape), q.device, workspace)
+    # one checked call establishes outputs and validates everything; then freeze the arguments
+    out, lse = _attn(tree, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, ws,
+                     sm_scale, split_keys, stream, lse is not None)
+    if cap == 0:
+        k_ctx = v_ctx = None
+    args = [ctypes.byref(shape), _ptr(q), _ptr(k_ctx), _ptr(v_ctx), _ptr(k_new), _ptr(v_new),
+            _ptr(ctx_lens)]
+    if tree:
+        args += [_ptr(parents)]
+    args += [_ptr(out), _ptr(lse), _ptr(ws), ctypes.c_size_t(ws.numel() * ws.element_size()),
+             _stream(stream)]
+    fn = lib().glance_tree_verify_attn if tree else lib().glance_block_draft_attn
+    keep = (shape, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, ws)
+    return PreparedCall(fn, args, keep), out, lse
+
+
+def prepare_block_draft_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, out=None, lse=None, workspace=None,
+                             sm_scale=0.0, split_keys=0, stream=None):
+    """Returns (call, out, lse): call() re-runs the draft attention into out / lse."""
+    return _prepare_attn(False, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, None, out, lse, workspace,
+                         sm_scale, split_keys, stream)
+
+
+def prepare_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out=None, lse=None,
+                             workspace=None, sm_scale=0.0, split_keys=0, stream=None):
+    """Returns (call, out, lse): call() re-runs the tree-verify attention into out / lse."""
+    return _prepare_attn(True, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, workspace,
+                         sm_scale, split_keys, stream)
+
+
+def prepare_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None, workspace=None,
+                          stream=None):
+    """Returns (call, outputs): call() re-runs the acceptance into the outputs dict."""
+    batch, n, vocab = logits.shape
+    ws = _workspace(glance_accept_workspace_size(batch, n, vocab), logits.device, workspace)
+    outputs = glance_greedy_accept(logits, parents, tokens, path_stride, outputs, ws, stream)
+    path_stride = int(path_stride or n)
+    args = [ctypes.c_int32(batch), ctypes.c_int32(n), ctypes.c_int32(vocab), ctypes.c_int(_dtype_code(logits)),
+            _ptr(logits), _ptr(parents), _ptr(tokens), _ptr(outputs["argmax"]), _ptr(outputs["accept_len"]),
+            _ptr(outputs["accept_path"]), ctypes.c_int32(path_stride), _ptr(outputs["next_root"]), _ptr(ws),
+            ctypes.c_size_t(ws.numel() * ws.element_size()), _stream(stream)]
+    keep = (logits, parents, tokens, outputs, ws)
+    return PreparedCall(lib().glance_greedy_accept, args, keep), outputs

@@ -1,0 +1,334 @@
+// C-ABI host layer: argument checks, split-KV planning, workspace layout and
+// kernel launches for the GLANCE round hot path (see include/glance.h).
+#include "glance.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "glance_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+thread_local hipEvent_t g_ev_start = nullptr;
+thread_local hipEvent_t g_ev_stop = nullptr;
+
+glance_status fail(glance_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+glance_status fail(glance_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+glance_status ok() { return GLANCE_OK; }
+
+bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Default split size: aim at about four workgroups per compute unit over the
+// whole grid, with at least 256 and at most 8192 context keys per split.
+int auto_split_keys(const glance_attn_shape& s, int row_groups) {
+  const long long target_wgs = 1024;
+  const long long cap = s.ctx_capacity > 0 ? s.ctx_capacity : 1;
+  long long per = cap * s.batch * s.n_kv_heads * row_groups / target_wgs;
+  per = (per + glance::kKeyTile - 1) / glance::kKeyTile * glance::kKeyTile;
+  if (per < 256) per = 256;
+  if (per > 8192) per = 8192;
+  return (int)per;
+}
+
+struct Plan {
+  glance::AttnParams p;
+  size_t part_o_bytes;
+  size_t part_ml_bytes;
+  size_t total;
+};
+
+glance_status check_shape(const glance_attn_shape* s) {
+  if (!s) return fail(GLANCE_ERR_INVALID_ARG, "shape is NULL");
+  if (s->batch < 1) return fail(GLANCE_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", s->batch);
+  if (s->n_new < 1 || s->n_new > 64)
+    return fail(GLANCE_ERR_UNSUPPORTED, "n_new must be in 1..64 (got %d)", s->n_new);
+  if (s->n_kv_heads < 1) return fail(GLANCE_ERR_INVALID_ARG, "n_kv_heads must be >= 1");
+  if (s->n_q_heads < 1 || s->n_q_heads % s->n_kv_heads != 0)
+    return fail(GLANCE_ERR_INVALID_ARG, "n_q_heads (%d) must be a positive multiple of n_kv_heads (%d)",
+                s->n_q_heads, s->n_kv_heads);
+  if (s->n_q_heads / s->n_kv_heads > 16)
+    return fail(GLANCE_ERR_UNSUPPORTED, "at most 16 query heads per KV head (got %d)",
+                s->n_q_heads / s->n_kv_heads);
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return fail(GLANCE_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", s->head_dim);
+  if (s->ctx_capacity < 0) return fail(GLANCE_ERR_INVALID_ARG, "ctx_capacity must be >= 0");
+  if (s->dtype != GLANCE_F32 && s->dtype != GLANCE_BF16)
+    return fail(GLANCE_ERR_UNSUPPORTED, "dtype must be GLANCE_F32 or GLANCE_BF16");
+  if (s->split_keys < 0 || s->split_keys % glance::kKeyTile != 0)
+    return fail(GLANCE_ERR_INVALID_ARG, "split_keys must be 0 or a positive multiple of %d (got %d)",
+                glance::kKeyTile, s->split_keys);
+  if (!(s->sm_scale == s->sm_scale) || isinf(s->sm_scale))
+    return fail(GLANCE_ERR_INVALID_ARG, "sm_scale must be finite");
+  // index arithmetic in the kernels: element offsets fit in 64 bits, per-tensor
+  // row counts in 32 bits
+  const long long rows = (long long)s->batch * s->n_new * s->n_q_heads;
+  if (rows > 0x3fffffffLL) return fail(GLANCE_ERR_UNSUPPORTED, "batch * n_new * n_q_heads too large");
+  return ok();
+}
+
+glance_status make_plan(const glance_attn_shape* s, Plan* out) {
+  glance_status st = check_shape(s);
+  if (st != GLANCE_OK) return st;
+  glance::AttnParams p = {};
+  p.batch = s->batch;
+  p.n = s->n_new;
+  p.hq = s->n_q_heads;
+  p.hkv = s->n_kv_heads;
+  p.group = s->n_q_heads / s->n_kv_heads;
+  p.cap = s->ctx_capacity;
+  p.d = s->head_dim;
+  p.rows = p.n * p.group;
+  const int rb = s->dtype == GLANCE_BF16 ? glance::kBf16RowBlock : glance::kF32RowBlock;
+  p.row_groups = (p.rows + rb - 1) / rb;
+  p.rows_pad = p.row_groups * rb;
+  p.split_keys = s->split_keys > 0 ? s->split_keys : auto_split_keys(*s, p.row_groups);
+  p.nsplit = p.cap > 0 ? (p.cap + p.split_keys - 1) / p.split_keys : 1;
+  const float scale = s->sm_scale > 0.f ? s->sm_scale : 1.0f / sqrtf((float)s->head_dim);
+  p.scale_log2 = scale * 1.4426950408889634f;
+  const size_t slots = (size_t)p.batch * p.hkv * p.nsplit * p.rows_pad;
+  Plan pl;
+  pl.part_o_bytes = round_up(slots * p.d * sizeof(float), 256);
+  pl.part_ml_bytes = round_up(slots * sizeof(float2), 256);
+  pl.total = pl.part_o_bytes + pl.part_ml_bytes;
+  pl.p = p;
+  *out = pl;
+  return ok();
+}
+
+glance_status check_hip(hipError_t e, const char* what) {
+  if (e == hipSuccess) return GLANCE_OK;
+  return fail(GLANCE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+void take_events(hipEvent_t* a, hipEvent_t* b) {
+  *a = g_ev_start;
+  *b = g_ev_stop;
+  g_ev_start = g_ev_stop = nullptr;
+}
+
+glance_status attn_common(bool tree, const glance_attn_shape* s, const void* q, const void* k_ctx,
+                          const void* v_ctx, const void* k_new, const void* v_new,
+                          const int32_t* ctx_lens, const int32_t* parents, void* out, float* lse,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  Plan pl;
+  glance_status st = make_plan(s, &pl);
+  if (st != GLANCE_OK) return st;
+  struct {
+    const void* ptr;
+    const char* name;
+    bool need;
+  } req[] = {{q, "q", true},           {k_new, "k_new", true},        {v_new, "v_new", true},
+             {ctx_lens, "ctx_lens", true}, {out, "out", true},
+             {k_ctx, "k_ctx", s->ctx_capacity > 0}, {v_ctx, "v_ctx", s->ctx_capacity > 0},
+             {parents, "parents", tree}};
+  for (auto& r : req) {
+    if (r.need && !r.ptr) return fail(GLANCE_ERR_INVALID_ARG, "%s is NULL", r.name);
+    if (r.ptr && !aligned16(r.ptr) && r.ptr != ctx_lens && r.ptr != parents)
+      return fail(GLANCE_ERR_INVALID_ARG, "%s is not 16-byte aligned", r.name);
+  }
+  if ((reinterpret_cast<uintptr_t>(ctx_lens) & 3u) || (parents && (reinterpret_cast<uintptr_t>(parents) & 3u)))
+    return fail(GLANCE_ERR_INVALID_ARG, "int32 arrays must be 4-byte aligned");
+  if (lse && (reinterpret_cast<uintptr_t>(lse) & 3u))
+    return fail(GLANCE_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  if (!workspace) return fail(GLANCE_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(GLANCE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < pl.total)
+    return fail(GLANCE_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes,
+                pl.total);
+
+  glance::AttnParams p = pl.p;
+  p.q = q;
+  p.k_ctx = k_ctx;
+  p.v_ctx = v_ctx;
+  p.k_new = k_new;
+  p.v_new = v_new;
+  p.ctx_lens = ctx_lens;
+  p.parents = tree ? parents : nullptr;
+  p.part_o = static_cast<float*>(workspace);
+  p.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + pl.part_o_bytes);
+  p.out = out;
+  p.lse = lse;
+  hipEvent_t e0, e1;
+  take_events(&e0, &e1);
+  const bool bf16 = s->dtype == GLANCE_BF16;
+  hipError_t e = bf16 ? glance::launch_attn_bf16(p, tree, stream, e0, e1)
+                      : glance::launch_attn_f32(p, tree, stream, e0, e1);
+  if ((st = check_hip(e, "attention kernel launch")) != GLANCE_OK) return st;
+  e = glance::launch_attn_merge(p, bf16, stream);
+  return check_hip(e, "merge kernel launch");
+}
+
+struct AcceptPlan {
+  int chunks, chunk_len;
+  size_t bytes;
+};
+
+glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptPlan* out) {
+  if (batch < 1) return fail(GLANCE_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (n_nodes < 1 || n_nodes > 64)
+    return fail(GLANCE_ERR_UNSUPPORTED, "n_nodes must be in 1..64 (got %d)", n_nodes);
+  if (vocab < 1 || vocab > (1 << 30)) return fail(GLANCE_ERR_INVALID_ARG, "vocab must be in 1..2^30");
+  const long long rows = (long long)batch * n_nodes;
+  if (rows * (long long)vocab > (1LL << 40)) return fail(GLANCE_ERR_UNSUPPORTED, "logits too large");
+  // about 2048 workgroups over the grid, chunks of at least 4096 values
+  long long chunks = (2048 + rows - 1) / rows;
+  long long max_chunks = ((long long)vocab + 4095) / 4096;
+  if (chunks > max_chunks) chunks = max_chunks;
+  if (chunks < 1) chunks = 1;
+  long long len = ((long long)vocab + chunks - 1) / chunks;
+  len = (len + 7) / 8 * 8;
+  chunks = ((long long)vocab + len - 1) / len;
+  out->chunks = (int)chunks;
+  out->chunk_len = (int)len;
+  out->bytes = round_up((size_t)rows * chunks * sizeof(unsigned long long), 256);
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+glance_status glance_block_draft_attn(const glance_attn_shape* s, const void* q, const void* k_ctx,
+                                      const void* v_ctx, const void* k_new, const void* v_new,
+                                      const int32_t* ctx_lens, void* out, float* lse,
+                                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return attn_common(false, s, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, nullptr, out, lse, workspace,
+                     workspace_bytes, stream);
+}
+
+glance_status glance_tree_verify_attn(const glance_attn_shape* s, const void* q, const void* k_ctx,
+                                      const void* v_ctx, const void* k_new, const void* v_new,
+                                      const int32_t* ctx_lens, const int32_t* parents, void* out,
+                                      float* lse, void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream) {
+  return attn_common(true, s, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, workspace,
+                     workspace_bytes, stream);
+}
+
+glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                   glance_dtype logits_dtype, const void* logits,
+                                   const int32_t* parents, const int32_t* tokens,
+                                   int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
+                                   int32_t path_stride, int32_t* next_root, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
+  AcceptPlan pl;
+  glance_status st = accept_plan(batch, n_nodes, vocab, &pl);
+  if (st != GLANCE_OK) return st;
+  if (logits_dtype != GLANCE_F32 && logits_dtype != GLANCE_BF16)
+    return fail(GLANCE_ERR_UNSUPPORTED, "logits dtype must be GLANCE_F32 or GLANCE_BF16");
+  if (path_stride < 1) return fail(GLANCE_ERR_INVALID_ARG, "path_stride must be >= 1");
+  struct {
+    const void* ptr;
+    const char* name;
+  } req[] = {{logits, "logits"},         {parents, "parents"},         {tokens, "tokens"},
+             {argmax_out, "argmax_out"}, {accept_len, "accept_len"}, {accept_path, "accept_path"},
+             {next_root, "next_root"}};
+  for (auto& r : req) {
+    if (!r.ptr) return fail(GLANCE_ERR_INVALID_ARG, "%s is NULL", r.name);
+    if (reinterpret_cast<uintptr_t>(r.ptr) & 3u) return fail(GLANCE_ERR_INVALID_ARG, "%s is not 4-byte aligned", r.name);
+  }
+  if (logits_dtype == GLANCE_BF16 && (reinterpret_cast<uintptr_t>(logits) & 1u))
+    return fail(GLANCE_ERR_INVALID_ARG, "logits is not 2-byte aligned");
+  if (!workspace) return fail(GLANCE_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(GLANCE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < pl.bytes)
+    return fail(GLANCE_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes,
+                pl.bytes);
+  glance::AcceptParams p = {};
+  p.logits = logits;
+  p.parents = parents;
+  p.tokens = tokens;
+  p.argmax_out = argmax_out;
+  p.accept_len = accept_len;
+  p.accept_path = accept_path;
+  p.next_root = next_root;
+  p.part = static_cast<unsigned long long*>(workspace);
+  p.batch = batch;
+  p.n_nodes = n_nodes;
+  p.vocab = vocab;
+  p.path_stride = path_stride;
+  p.chunks = pl.chunks;
+  p.chunk_len = pl.chunk_len;
+  hipEvent_t e0, e1;
+  take_events(&e0, &e1);
+  return check_hip(glance::launch_accept(p, logits_dtype == GLANCE_BF16, stream, e0, e1),
+                   "accept kernel launch");
+}
+
+size_t glance_attn_workspace_size(const glance_attn_shape* s) {
+  Plan pl;
+  if (make_plan(s, &pl) != GLANCE_OK) return 0;
+  return pl.total;
+}
+
+size_t glance_accept_workspace_size(int32_t batch, int32_t n_nodes, int32_t vocab) {
+  AcceptPlan pl;
+  if (accept_plan(batch, n_nodes, vocab, &pl) != GLANCE_OK) return 0;
+  return pl.bytes;
+}
+
+glance_status glance_validate_tree(int32_t n, const int32_t* parents, const int32_t* tokens,
+                                   int32_t max_depth) {
+  if (n < 1 || n > 64) return fail(GLANCE_ERR_INVALID_ARG, "tree size must be in 1..64 (got %d)", n);
+  if (!parents) return fail(GLANCE_ERR_INVALID_ARG, "parents is NULL");
+  if (parents[0] != -1) return fail(GLANCE_ERR_INVALID_ARG, "parents[0] must be -1 (got %d)", parents[0]);
+  int depth[64];
+  depth[0] = 0;
+  for (int i = 1; i < n; ++i) {
+    if (parents[i] < 0 || parents[i] >= i)
+      return fail(GLANCE_ERR_INVALID_ARG, "parents[%d] = %d is not in [0, %d)", i, parents[i], i);
+    depth[i] = depth[parents[i]] + 1;
+    if (max_depth >= 0 && depth[i] > max_depth)
+      return fail(GLANCE_ERR_INVALID_ARG, "node %d has depth %d > %d", i, depth[i], max_depth);
+  }
+  if (tokens) {
+    for (int i = 1; i < n; ++i)
+      for (int j = 1; j < i; ++j)
+        if (parents[j] == parents[i] && tokens[j] == tokens[i])
+          return fail(GLANCE_ERR_INVALID_ARG, "siblings %d and %d carry the same token %d", j, i, tokens[i]);
+  }
+  return ok();
+}
+
+const char* glance_status_string(glance_status status) {
+  switch (status) {
+    case GLANCE_OK: return "ok";
+    case GLANCE_ERR_INVALID_ARG: return "invalid argument";
+    case GLANCE_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case GLANCE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case GLANCE_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* glance_last_error(void) { return g_last_error.c_str(); }
+
+glance_status glance_set_kernel_events(void* start_event, void* stop_event) {
+  if ((start_event == nullptr) != (stop_event == nullptr))
+    return fail(GLANCE_ERR_INVALID_ARG, "pass both events or neither");
+  g_ev_start = static_cast<hipEvent_t>(start_event);
+  g_ev_stop = static_cast<hipEvent_t>(stop_event);
+  return ok();
+}
+
+int32_t glance_version(void) { return 100; }
+
+}  // extern "C"

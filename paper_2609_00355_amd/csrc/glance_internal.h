@@ -1,0 +1,67 @@
+// Internal interface between the C-ABI host layer and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace glance {
+
+// Keys per LDS tile and waves per workgroup of the attention kernels.
+constexpr int kKeyTile = 64;
+constexpr int kWaves = 4;
+// Rows per workgroup of the fp32 attention kernel (kWaves waves x 8 rows).
+constexpr int kF32RowsPerWave = 8;
+constexpr int kF32RowBlock = kWaves * kF32RowsPerWave;
+// Row tiles per wave of the bf16 MFMA kernel (16 rows per tile).
+constexpr int kBf16TilesPerWave = 2;
+constexpr int kBf16RowBlock = kWaves * kBf16TilesPerWave * 16;
+
+// Everything a split-KV attention launch needs.  Layouts:
+//   q      [batch][n][hq][d]         k_ctx/v_ctx [batch][hkv][cap][d]
+//   k_new  [batch][n][hkv][d]        parents [batch][n]
+//   part_o [batch][hkv][nsplit][rows_pad][d] f32 (unnormalised partial output)
+//   part_ml[batch][hkv][nsplit][rows_pad]    f32x2 (running max * scale*log2e, sum)
+//   out    [batch][n][hq][d]         lse [batch][n][hq]
+// Row r of a (sequence, KV head) problem is new row r / group of query head
+// g * group + r % group.
+struct AttnParams {
+  const void* q;
+  const void* k_ctx;
+  const void* v_ctx;
+  const void* k_new;
+  const void* v_new;
+  const int32_t* ctx_lens;
+  const int32_t* parents;  // null for the block draft
+  float* part_o;
+  float2* part_ml;
+  void* out;
+  float* lse;
+  int batch, n, hq, hkv, group, cap, d;
+  int rows;       // n * group
+  int rows_pad;   // rows rounded up to the kernel's row block
+  int row_groups; // workgroups sharing one KV split (rows_pad / row block)
+  int nsplit;     // split slots per (sequence, KV head) = ceil(cap / split_keys), >= 1
+  int split_keys; // context keys per split, multiple of kKeyTile
+  float scale_log2;  // sm_scale * log2(e)
+};
+
+struct AcceptParams {
+  const void* logits;
+  const int32_t* parents;
+  const int32_t* tokens;
+  int32_t* argmax_out;
+  int32_t* accept_len;
+  int32_t* accept_path;
+  int32_t* next_root;
+  unsigned long long* part;  // [batch * n_nodes][chunks] packed (key, ~index)
+  int batch, n_nodes, vocab, path_stride;
+  int chunks, chunk_len;     // chunk_len is a multiple of 8
+};
+
+hipError_t launch_attn_bf16(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+hipError_t launch_attn_f32(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+hipError_t launch_attn_merge(const AttnParams& p, bool out_bf16, hipStream_t s);
+hipError_t launch_accept(const AcceptParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+
+}  // namespace glance

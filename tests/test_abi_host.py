@@ -1,0 +1,158 @@
+"""C-ABI boundary checks that need no GPU: the library loads, exports every
+symbol include/glance.h declares, and rejects bad arguments on the host before
+any HIP call.  Every call made here fails validation (at least one argument is
+invalid), so no kernel is ever launched with the placeholder pointers used."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_00355_amd as G
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "glance.h")
+
+FAKE = ctypes.c_void_p(0x10000)   # aligned placeholder; never dereferenced (validation fails first)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(G.LIB_PATH):
+        from paper_2609_00355_amd import build
+        build.build()
+    return G.lib()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(glance_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in glance.h but not exported"
+
+
+def test_version_and_status_strings(lib):
+    assert G.glance_version() >= 100
+    for code in (0, -1, -2, -3, -4):
+        assert G.glance_status_string(code)
+    assert G.glance_status_string(7) == "unknown status"
+
+
+def _shape(**kw):
+    base = dict(batch=1, n_new=16, n_q_heads=28, n_kv_heads=4, head_dim=128, ctx_capacity=2048,
+                dtype=G.GLANCE_BF16)
+    base.update(kw)
+    return G.attn_shape(**base)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(batch=0), G.GLANCE_ERR_INVALID_ARG),
+    (dict(n_new=0), G.GLANCE_ERR_UNSUPPORTED),
+    (dict(n_new=65), G.GLANCE_ERR_UNSUPPORTED),
+    (dict(n_q_heads=27), G.GLANCE_ERR_INVALID_ARG),
+    (dict(n_q_heads=68, n_kv_heads=4), G.GLANCE_ERR_UNSUPPORTED),
+    (dict(head_dim=96), G.GLANCE_ERR_UNSUPPORTED),
+    (dict(ctx_capacity=-1), G.GLANCE_ERR_INVALID_ARG),
+    (dict(dtype=5), G.GLANCE_ERR_UNSUPPORTED),
+    (dict(split_keys=100), G.GLANCE_ERR_INVALID_ARG),
+])
+def test_bad_shapes_are_rejected(lib, kw, code):
+    s = _shape(**kw)
+    assert G.glance_attn_workspace_size(s) == 0
+    st = lib.glance_block_draft_attn(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                     None, 0, None)
+    assert st == code, G.glance_last_error()
+    assert G.glance_last_error()
+
+
+def test_null_and_misaligned_pointers(lib):
+    s = _shape()
+    ws = G.glance_attn_workspace_size(s)
+    assert ws > 0
+    st = lib.glance_block_draft_attn(ctypes.byref(s), None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                     FAKE, ws, None)
+    assert st == G.GLANCE_ERR_INVALID_ARG and "q" in G.glance_last_error()
+    st = lib.glance_block_draft_attn(ctypes.byref(s), ctypes.c_void_p(0x10008), FAKE, FAKE, FAKE, FAKE,
+                                     FAKE, FAKE, None, FAKE, ws, None)
+    assert st == G.GLANCE_ERR_INVALID_ARG and "aligned" in G.glance_last_error()
+    st = lib.glance_tree_verify_attn(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                     None, FAKE, ws, None)
+    assert st == G.GLANCE_ERR_INVALID_ARG and "parents" in G.glance_last_error()
+
+
+def test_workspace_checks(lib):
+    s = _shape()
+    ws = G.glance_attn_workspace_size(s)
+    st = lib.glance_block_draft_attn(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                     None, ws, None)
+    assert st == G.GLANCE_ERR_WORKSPACE
+    st = lib.glance_block_draft_attn(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                     FAKE, ws - 1, None)
+    assert st == G.GLANCE_ERR_WORKSPACE and "too small" in G.glance_last_error()
+    st = lib.glance_block_draft_attn(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                     ctypes.c_void_p(0x10010), ws, None)
+    assert st == G.GLANCE_ERR_WORKSPACE and "256" in G.glance_last_error()
+
+
+def test_workspace_size_scales_with_splits(lib):
+    a = G.glance_attn_workspace_size(_shape(split_keys=1024))
+    b = G.glance_attn_workspace_size(_shape(split_keys=512))
+    assert b > a > 0
+    # partial outputs dominate: splits x rows x head_dim x 4 bytes
+    assert a >= 2 * 112 * 128 * 4
+
+
+def test_accept_argument_checks(lib):
+    assert G.glance_accept_workspace_size(4, 64, 152064) > 0
+    assert G.glance_accept_workspace_size(0, 64, 10) == 0
+    assert G.glance_accept_workspace_size(1, 65, 10) == 0
+    st = lib.glance_greedy_accept(1, 65, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16, FAKE,
+                                  FAKE, 1 << 20, None)
+    assert st == G.GLANCE_ERR_UNSUPPORTED
+    st = lib.glance_greedy_accept(1, 8, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, FAKE,
+                                  FAKE, 1 << 20, None)
+    assert st == G.GLANCE_ERR_INVALID_ARG and "path_stride" in G.glance_last_error()
+    st = lib.glance_greedy_accept(1, 8, 100, G.GLANCE_BF16, FAKE, None, FAKE, FAKE, FAKE, FAKE, 8, FAKE,
+                                  FAKE, 1 << 20, None)
+    assert st == G.GLANCE_ERR_INVALID_ARG and "parents" in G.glance_last_error()
+    st = lib.glance_greedy_accept(1, 8, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8, FAKE,
+                                  FAKE, 1, None)
+    assert st == G.GLANCE_ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("parents,tokens,max_depth,ok", [
+    ([-1], None, 15, True),
+    ([-1, 0, 0, 1, 3], [9, 1, 2, 3, 4], 15, True),
+    ([0, 0], None, 15, False),                 # root must have parent -1
+    ([-1, 1], None, 15, False),                # parent must precede the child
+    ([-1, 0, 3, 0], None, 15, False),
+    ([-1, 0, 1, 2, 3], None, 3, False),        # depth 4 > 3
+    ([-1, 0, 0], [5, 7, 7], 15, False),        # siblings repeat a token
+    ([-1, 0, 1], [5, 7, 7], 15, True),         # same token at different depths is fine
+])
+def test_validate_tree(lib, parents, tokens, max_depth, ok):
+    good, msg = G.glance_validate_tree(parents, tokens, max_depth)
+    assert good == ok, msg
+    if not ok:
+        assert msg
+
+
+def test_validate_generated_trees(lib):
+    from workloads import configs
+    w = configs.WORKLOADS["verify_4k"]
+    par, tok = configs.tree_inputs(w, seed=3)
+    good, msg = G.glance_validate_tree(par[0].numpy(), tok[0].numpy(), 15)
+    assert good, msg
+
+
+def test_kernel_events_need_both_or_neither(lib):
+    assert lib.glance_set_kernel_events(FAKE, None) == G.GLANCE_ERR_INVALID_ARG
+    assert lib.glance_set_kernel_events(None, None) == G.GLANCE_OK

@@ -1,0 +1,133 @@
+"""Bit-exact parity of the HIP greedy acceptance with the oracle: argmax of
+every row (lowest index on ties), accepted length, accepted path and the
+bonus token, on planted logits, tie fixtures and edge cases."""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import assert_accept_equal, ensure_lib, run_accept
+from workloads import configs as C
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    ensure_lib()
+
+
+def _round(name, seed=0, batch=None):
+    w = C.WORKLOADS[name]
+    if batch is not None:
+        w = C.custom_workload(name, batch=batch)
+    par, tok = C.tree_inputs(w, seed)
+    logits = C.planted_logits(w, par, tok, seed)
+    return logits, par, tok
+
+
+@pytest.mark.parametrize("name", ["tiny_fp32", "verify_4k"])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_planted_rounds(name, seed):
+    logits, par, tok = _round(name, seed)
+    got = run_accept(logits, par, tok, path_stride=16)
+    ref = assert_accept_equal(got, logits, par, tok, path_stride=16)
+    print(f"[{name} seed {seed}] accept_len={ref['accept_len'].tolist()}", flush=True)
+
+
+def test_doc_16k_and_ragged_mix_logits():
+    for name in ("doc_16k", "ragged_mix"):
+        logits, par, tok = _round(name, 0)
+        got = run_accept(logits, par, tok, path_stride=16)
+        ref = assert_accept_equal(got, logits, par, tok, path_stride=16)
+        print(f"[{name}] mean accept_len={ref['accept_len'].mean():.2f}", flush=True)
+
+
+def _tie_logits(vocab, dtype, ties, batch=1, n=4):
+    """Rows of N(0,1) with the maximum value 9.0 planted at every index in ``ties``."""
+    g = torch.Generator().manual_seed(1234)
+    x = torch.randn((batch, n, vocab), generator=g)
+    for b in range(batch):
+        for v in range(n):
+            for j in ties:
+                x[b, v, j] = 9.0
+    return x.to(dtype)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("ties", [(0, 152063), (5, 6), (4095, 4096), (70000, 8, 152000), (151999,)])
+def test_ties_resolve_to_lowest_index(dtype, ties):
+    vocab = 152064
+    logits = _tie_logits(vocab, dtype, ties)
+    par = torch.tensor([[-1, 0, 0, 1]], dtype=torch.int32)
+    tok = torch.tensor([[3, min(ties), max(ties), 11]], dtype=torch.int32)
+    got = run_accept(logits, par, tok)
+    assert (got["argmax"] == min(ties)).all()
+    assert_accept_equal(got, logits, par, tok)
+
+
+@pytest.mark.parametrize("vocab", [1, 7, 1000, 4097, 152063])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_odd_vocab_sizes(vocab, dtype):
+    g = torch.Generator().manual_seed(vocab)
+    logits = torch.randn((2, 5, vocab), generator=g).to(dtype)
+    par = torch.tensor([[-1, 0, 1, 1, 0], [-1, 0, 0, 2, 3]], dtype=torch.int32)
+    am = logits.float().argmax(-1)
+    tok = torch.tensor([[0, int(am[0, 0]), int(am[0, 1]), 1, 2],
+                        [0, 5, int(am[1, 0]), int(am[1, 2]), int(am[1, 3])]], dtype=torch.int32)
+    got = run_accept(logits, par, tok)
+    assert_accept_equal(got, logits, par, tok)
+
+
+def test_signed_zero_and_nan_semantics():
+    vocab = 64
+    x = torch.full((1, 3, vocab), -1.0)
+    x[0, 0, 40] = -0.0
+    x[0, 0, 9] = 0.0            # -0 == +0: the lowest index (9) wins
+    x[0, 1, 50] = float("nan")
+    x[0, 1, 20] = float("nan")  # first NaN wins
+    x[0, 1, 3] = 100.0
+    x[0, 2, 33] = -float("nan")  # negative-signed NaN still counts as the maximum
+    x[0, 2, 2] = float("inf")
+    par = torch.tensor([[-1, 0, 1]], dtype=torch.int32)
+    tok = torch.tensor([[0, 9, 20]], dtype=torch.int32)
+    for dtype in (torch.float32, torch.bfloat16):
+        logits = x.to(dtype)
+        got = run_accept(logits, par, tok)
+        assert got["argmax"].tolist() == [[9, 20, 33]]
+        assert_accept_equal(got, logits, par, tok)
+        assert got["accept_len"].tolist() == [2]
+
+
+def test_path_stride_truncates_but_counts():
+    n = 20
+    par = torch.arange(-1, n - 1, dtype=torch.int32)[None]
+    tok = torch.arange(100, 100 + n, dtype=torch.int32)[None]
+    logits = torch.zeros((1, n, 200))
+    for v in range(n - 1):
+        logits[0, v, 100 + v + 1] = 1.0
+    got = run_accept(logits, par, tok, path_stride=5)
+    assert got["accept_len"].tolist() == [n - 1]
+    assert got["accept_path"].tolist() == [[0, 1, 2, 3, 4]]
+    assert got["next_root"].tolist() == [0]
+
+
+def test_malformed_parents_terminate():
+    """Parents that point forward or out of range end the walk instead of looping."""
+    par = torch.tensor([[-1, 0, 5, 1, 99, 2]], dtype=torch.int32)
+    tok = torch.tensor([[0, 1, 2, 3, 4, 5]], dtype=torch.int32)
+    logits = torch.zeros((1, 6, 8))
+    for v in range(6):
+        logits[0, v, (v + 1) % 8] = 1.0
+    got = run_accept(logits, par, tok)
+    # row 0 -> token 1 -> node 1; row 1 -> token 2: node 2's parent is 5 (not 1), so stop
+    assert got["accept_len"].tolist() == [1]
+    assert got["next_root"].tolist() == [2]
+
+
+def test_many_sequences():
+    w = C.custom_workload("tiny_fp32", batch=37)
+    par, tok = C.tree_inputs(w, 6)
+    logits = C.planted_logits(w, par, tok, 6)
+    got = run_accept(logits, par, tok, path_stride=16)
+    assert_accept_equal(got, logits, par, tok, path_stride=16)

@@ -1,0 +1,174 @@
+"""Parity of the HIP draft / verify attention with the float64 oracle.
+
+Element-by-element on every output at oracle-sized shapes that span several
+key tiles, several splits and a ragged tail; sampled rows at the full
+workload sizes, in the launch configuration the benchmark times.  Inputs come
+from the seeded generators in ``workloads`` and are fed unchanged to both sides.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_00355_amd as G
+from gpu_helpers import assert_close, ensure_lib, oracle_attention, run_attention
+from workloads import configs as C
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    ensure_lib()
+
+
+def _w(name, **kw):
+    return C.custom_workload(name, **kw)
+
+
+def _check(kind, w, ctx_lens, n, seed=0, variant=None, poison=False, tree_shape="best_first",
+           split_keys=0, cap=None, what=""):
+    inp = C.attention_inputs(w, kind, n, ctx_lens, seed, variant, poison, cap=cap)
+    par = None
+    if kind == "verify":
+        par, _ = C.tree_inputs(w, seed, tree_shape, n=n, batch=len(ctx_lens))
+    out, lse = run_attention(kind, inp, par, split_keys=split_keys)
+    ref_out, ref_lse = oracle_attention(kind, inp, par)
+    print(f"[{what}] {kind} n={n} ctx={list(ctx_lens)[:4]} variant={variant}", flush=True)
+    return assert_close(out, lse, ref_out, ref_lse, w.dtype, what)
+
+
+# ------------------------------------------------------------- fp32 (VALU path)
+def test_tiny_fp32_draft_and_verify():
+    w = C.WORKLOADS["tiny_fp32"]
+    ctx = C.context_lengths(w)
+    _check("draft", w, ctx, w.n_draft, what="tiny_fp32 draft")
+    _check("verify", w, ctx, w.n_tree, what="tiny_fp32 verify")
+
+
+@pytest.mark.parametrize("kind", ["draft", "verify"])
+@pytest.mark.parametrize("variant", [None, "sharp1", "sharp4", "tree_dominant"])
+def test_fp32_variants(kind, variant):
+    w = _w("tiny_fp32")
+    _check(kind, w, [300], 16, seed=1, variant=variant, poison=True, what=f"fp32 {variant}")
+
+
+@pytest.mark.parametrize("d,hq,hkv", [(64, 4, 1), (128, 8, 1), (64, 6, 3), (128, 16, 2)])
+@pytest.mark.parametrize("n", [1, 5, 64])
+def test_fp32_shapes(d, hq, hkv, n):
+    w = _w("tiny_fp32", d=d, hq=hq, hkv=hkv)
+    for kind in ("draft", "verify"):
+        _check(kind, w, [0, 65, 129], n, seed=2, variant="sharp1", poison=True, cap=200,
+               what=f"fp32 d{d} h{hq}/{hkv}")
+
+
+@pytest.mark.parametrize("shape", ["chain", "star", "best_first"])
+def test_fp32_tree_shapes(shape):
+    w = _w("tiny_fp32", n_tree=40, depth_cap=39)
+    _check("verify", w, [77, 0], 40, seed=3, variant="tree_dominant", tree_shape=shape,
+           what=f"fp32 {shape}")
+
+
+# ------------------------------------------------------------- bf16 (MFMA path)
+def test_draft_2k_full():
+    w = C.WORKLOADS["draft_2k"]
+    _check("draft", w, C.context_lengths(w), w.n_draft, what="draft_2k")
+
+
+def test_verify_4k_full():
+    w = C.WORKLOADS["verify_4k"]
+    _check("verify", w, C.context_lengths(w), w.n_tree, what="verify_4k")
+
+
+@pytest.mark.parametrize("kind", ["draft", "verify"])
+@pytest.mark.parametrize("variant", ["sharp1", "sharp4", "tree_dominant"])
+def test_bf16_sharp_variants(kind, variant):
+    w = _w("verify_4k")
+    n = 16 if kind == "draft" else 64
+    _check(kind, w, [1000, 37], n, seed=4, variant=variant, poison=True, cap=1100,
+           what=f"bf16 {variant}")
+
+
+@pytest.mark.parametrize("n", [1, 7, 16, 33, 64])
+@pytest.mark.parametrize("ctx", [[0], [1], [63, 64, 65], [700, 0, 1]])
+def test_bf16_rows_and_context_edges(n, ctx):
+    w = _w("verify_4k", batch=len(ctx))
+    for kind in ("draft", "verify"):
+        _check(kind, w, ctx, n, seed=5, variant="sharp1", poison=True, cap=max(max(ctx), 1) + 5,
+               what=f"bf16 edges n={n}")
+
+
+@pytest.mark.parametrize("d,hq,hkv", [(64, 28, 4), (128, 8, 1), (128, 16, 2), (128, 4, 4)])
+def test_bf16_head_shapes(d, hq, hkv):
+    w = _w("verify_4k", d=d, hq=hq, hkv=hkv)
+    for kind in ("draft", "verify"):
+        _check(kind, w, [513, 90], 24, seed=6, variant="sharp1", poison=True, cap=600,
+               what=f"bf16 d{d} h{hq}/{hkv}")
+
+
+@pytest.mark.parametrize("shape", ["chain", "star"])
+def test_bf16_chain_and_star(shape):
+    w = _w("verify_4k", n_tree=64, depth_cap=63)
+    _check("verify", w, [200], 64, seed=7, variant="tree_dominant", tree_shape=shape,
+           what=f"bf16 {shape}")
+
+
+@pytest.mark.parametrize("split_keys", [64, 256, 1024, 0])
+def test_split_count_invariance(split_keys):
+    w = _w("verify_4k", batch=2)
+    for kind, n in (("draft", 16), ("verify", 64)):
+        _check(kind, w, [3000, 1234], n, seed=8, variant="sharp1", split_keys=split_keys, cap=3100,
+               what=f"split {split_keys}")
+
+
+def test_ragged_batch_small():
+    w = _w("verify_4k", batch=6)
+    ctx = [0, 1, 64, 1000, 2500, 3333]
+    for kind, n in (("draft", 16), ("verify", 64)):
+        _check(kind, w, ctx, n, seed=9, poison=True, cap=3400, what="ragged small")
+
+
+def test_deterministic_bitwise():
+    w = _w("verify_4k", batch=2)
+    inp = C.attention_inputs(w, "verify", 64, [2000, 999], 10, "sharp1", cap=2100)
+    par, _ = C.tree_inputs(w, 10, n=64, batch=2)
+    a = run_attention("verify", inp, par)
+    b = run_attention("verify", inp, par)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+
+
+def test_explicit_scale():
+    w = _w("verify_4k", batch=1)
+    inp = C.attention_inputs(w, "verify", 64, [500], 11, "sharp1", cap=500)
+    par, _ = C.tree_inputs(w, 11, n=64, batch=1)
+    out, lse = run_attention("verify", inp, par, sm_scale=0.02)
+    ref_out, ref_lse = oracle_attention("verify", inp, par, sm_scale=0.02)
+    assert_close(out, lse, ref_out, ref_lse, "bf16", "explicit scale")
+
+
+# ------------------------------------------------------------- full workload sizes (sampled rows)
+def _sampled_full(name, kind, seed=0):
+    w = C.WORKLOADS[name]
+    ctx = C.context_lengths(w, seed)
+    n = w.n_draft if kind == "draft" else w.n_tree
+    inp = C.attention_inputs(w, kind, n, ctx, seed, None, False, cap=w.cap)
+    par = None
+    if kind == "verify":
+        par, _ = C.tree_inputs(w, seed)
+    out, lse = run_attention(kind, inp, par)
+    rows = sorted({0, 1, n // 2, n - 1})
+    ref_out, ref_lse = oracle_attention(kind, inp, par, rows=rows)
+    print(f"[{name} {kind}] ctx={list(ctx)[:6]} rows={rows}", flush=True)
+    assert_close(out[:, rows], lse[:, rows], ref_out, ref_lse, w.dtype, f"{name} {kind} sampled")
+    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse))
+
+
+@pytest.mark.parametrize("kind", ["draft", "verify"])
+def test_doc_16k_full_size_sampled(kind):
+    _sampled_full("doc_16k", kind)
+
+
+@pytest.mark.parametrize("kind", ["draft", "verify"])
+def test_ragged_mix_full_size_sampled(kind):
+    _sampled_full("ragged_mix", kind)

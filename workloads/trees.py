@@ -23,25 +23,32 @@ def best_first_tree(n, depth_cap, branch_choices, vocab, key):
     The root has score 1.  Repeatedly the highest-score unexpanded node whose
     depth is below ``depth_cap`` (ties: lowest index) gets k children, k drawn
     from ``branch_choices``; child rank r gets score parent * c * 2**-r with
-    c ~ U(0.5, 0.95).  Nodes are numbered in creation order.
+    c ~ U(0.5, 0.95).  If every node below the cap is already expanded, the
+    best one gets one more child.  Nodes are numbered in creation order.
     """
     rng = _rng(*key)
-    parents, depth, score, expanded = [-1], [0], [1.0], [False]
+    parents, depth, score, expanded, nkids = [-1], [0], [1.0], [False], [0]
+    if n > 1 and depth_cap < 1:
+        raise ValueError("depth cap too small for the requested node count")
     while len(parents) < n:
         frontier = [i for i in range(len(parents)) if not expanded[i] and depth[i] < depth_cap]
-        if not frontier:
-            raise ValueError("depth cap too small for the requested node count")
-        v = max(frontier, key=lambda i: (score[i], -i))
-        expanded[v] = True
-        k = int(rng.choice(branch_choices))
-        for r in range(k):
+        if frontier:
+            v = max(frontier, key=lambda i: (score[i], -i))
+            expanded[v] = True
+            k = int(rng.choice(branch_choices))
+        else:  # every node below the cap is expanded: widen the best one by one more child
+            v = max((i for i in range(len(parents)) if depth[i] < depth_cap), key=lambda i: (score[i], -i))
+            k = 1
+        for _ in range(k):
             if len(parents) == n:
                 break
             c = rng.uniform(0.5, 0.95)
             parents.append(v)
             depth.append(depth[v] + 1)
-            score.append(score[v] * c * 2.0 ** (-r))
+            score.append(score[v] * c * 2.0 ** (-nkids[v]))
             expanded.append(False)
+            nkids.append(0)
+            nkids[v] += 1
     tokens = assign_tokens(parents, vocab, rng)
     return np.asarray(parents, dtype=np.int32), tokens
 
