@@ -6,9 +6,16 @@
 // K/V tile staged in LDS is shared by every query head of the GQA group and
 // by every block/tree row: the context is read from HBM once per split.
 //
-// Per 64-key LDS tile each wave computes, for each of its 16-row tiles,
-//   S^T[key][row] = K[key][:] . Q[row][:]      (v_mfma_f32_16x16x32_bf16, A = K, B = Q^T)
-//   online softmax over the keys of each row  (exp2 with the scale folded in)
+// K/V tiles of 64 keys stream from HBM straight into LDS (global_load_lds,
+// 16 bytes per lane, no register staging) through a ring of kStages buffers,
+// so several tiles are in flight per workgroup while the current one is
+// consumed.  Rows of the tile are stored unpadded with the 16-byte chunks of
+// key k permuted by an XOR with swz(k), which keeps both the K-operand reads
+// and the transposed V reads free of bank conflicts.
+//
+// Per tile each wave computes, for each of its 16-row tiles,
+//   S^T[key][row] = K[key][:] . Q[row][:]        (v_mfma_f32_16x16x32_bf16, A = K, B = Q^T)
+//   online softmax over the keys of each row    (exp2 with the scale folded in)
 //   O^T[d][row]  += V^T[d][key] . P^T[key][row] (A = V^T via ds_read_b64_tr_b16, B = P^T)
 // S^T is computed with the key order permuted inside each 32-key group so
 // that the MFMA result layout (lane l holds rows l%16, key slots 4*(l/16)+i)
@@ -22,6 +29,8 @@
 // combines the splits.
 #include "glance_internal.h"
 
+#include <type_traits>
+
 namespace glance {
 namespace {
 
@@ -30,31 +39,75 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr float kNegInf = -__builtin_inff();
+constexpr int kStages = 4;     // LDS ring depth: tiles in flight per workgroup
+constexpr float kSlack = 8.f;  // lazy-rescale threshold (exp2 units)
 
 template <int D>
-struct TileGeom {
-  static constexpr int kStride = D + 8;  // bf16 per LDS key row: 16-byte pad against bank conflicts
-  static constexpr int kChunks = D / 8;  // 16-byte chunks per key row
-  static constexpr int kLoads = kKeyTile * kChunks / (kWaves * 64);  // chunks per thread per tensor
+struct Geom {
+  static constexpr int kRowBytes = D * 2;                    // one key row, unpadded
+  static constexpr int kChunks = D / 8;                      // 16-byte chunks per row
+  static constexpr int kKeysPerInst = 64 / kChunks;          // rows filled by one wave load
+  static constexpr int kTileBytes = kKeyTile * kRowBytes;    // one K (or V) tile
+  static constexpr int kInstPerWave = kKeyTile / (kKeysPerInst * kBf16Waves);
 };
+
+// Chunk permutation of key row k (XOR, so a bijection on the chunks of a row).
+// Lanes 0-7 of a K-operand read touch rows {0-3, 8-11} (+16 for lanes 8-15) at
+// one chunk; lanes of a transposed V read touch 4 consecutive rows at two
+// neighbouring chunks.  Both land on distinct 16-byte bank groups.
+template <int D>
+__device__ __forceinline__ int swz(int k) {
+  int s = ((k & 3) << 1) | ((k >> 3) & 1);
+  if (D >= 128) s |= (k >> 1) & 8;
+  return s;
+}
+
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-template <int D, bool TREE>
-__global__ __launch_bounds__(kWaves * 64) void attn_bf16_partial(AttnParams p) {
-  constexpr int TPW = kBf16TilesPerWave;
+// Workgroup barrier for the DMA ring.  __syncthreads() carries a release fence,
+// which would make every wave wait for all of its outstanding global->LDS
+// loads (vmcnt(0)) and drain the ring.  Here each wave has already waited for
+// the loads of the tile it is about to read (wait_vmcnt), so the barrier only
+// has to order LDS: finish this wave's own LDS operations, then s_barrier.  The
+// "memory" clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int D, bool TREE, int TPW>
+__global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams p) {
+  using G_ = Geom<D>;
   constexpr int KS = D / 32;  // k-steps of Q.K^T
   constexpr int DT = D / 16;  // d-tiles of P.V
-  constexpr int ST = TileGeom<D>::kStride;
-  constexpr int CH = TileGeom<D>::kChunks;
-  constexpr int NL = TileGeom<D>::kLoads;
-  static_assert(NL * kWaves * 64 == kKeyTile * CH, "tile load must divide evenly");
+  constexpr int RB = G_::kRowBytes;
+  constexpr int CH = G_::kChunks;
+  constexpr int IPW = G_::kInstPerWave;
+  constexpr int LOADS_PER_TILE = 2 * IPW;  // K and V load instructions per wave per tile
+  static_assert(IPW * G_::kKeysPerInst * kBf16Waves == kKeyTile, "tile load must divide evenly");
 
-  __shared__ __attribute__((aligned(16))) __bf16 sK[2][kKeyTile * ST];
-  __shared__ __attribute__((aligned(16))) __bf16 sV[2][kKeyTile * ST];
+  // One LDS variable per ring stage and tensor, always addressed with a
+  // compile-time stage index: the compiler can then tell that reading stage A
+  // does not alias the DMA still landing in stage B, and waits only as told.
+  __shared__ __attribute__((aligned(1024))) char sK0[G_::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char sK1[G_::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char sK2[G_::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char sK3[G_::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char sV0[G_::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char sV1[G_::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char sV2[G_::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char sV3[G_::kTileBytes];
   __shared__ unsigned long long sAnc[64];
+  static_assert(kStages == 4, "one LDS variable per stage");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -87,10 +140,57 @@ __global__ __launch_bounds__(kWaves * 64) void attn_bf16_partial(AttnParams p) {
   const int n_tiles = n_ctx_tiles + (has_new ? 1 : 0);
 
   const __bf16* q = static_cast<const __bf16*>(p.q);
-  const __bf16* kc = static_cast<const __bf16*>(p.k_ctx);
-  const __bf16* vc = static_cast<const __bf16*>(p.v_ctx);
-  const __bf16* kn = static_cast<const __bf16*>(p.k_new);
-  const __bf16* vn = static_cast<const __bf16*>(p.v_new);
+  const char* kc = static_cast<const char*>(p.k_ctx);
+  const char* vc = static_cast<const char*>(p.v_ctx);
+  const char* kn = static_cast<const char*>(p.k_new);
+  const char* vn = static_cast<const char*>(p.v_new);
+
+  // ---- issue the loads of tile t into ring stage st.  Wave w fills rows
+  // [8w, 8w+8); lane i of a load writes LDS row base + i/CH, chunk slot i%CH,
+  // which holds global chunk slot ^ swz(row).  Rows past the valid keys re-read
+  // the last valid row: their scores are masked, so P = 0 and V is finite.
+  auto issue = [&](int t, auto stage) {
+    constexpr int st = decltype(stage)::value;
+    char* dK = st == 0 ? sK0 : st == 1 ? sK1 : st == 2 ? sK2 : sK3;
+    char* dV = st == 0 ? sV0 : st == 1 ? sV1 : st == 2 ? sV2 : sV3;
+    const char* kb;
+    const char* vb;
+    size_t stride;
+    int nvalid;
+    if (t < n_ctx_tiles) {
+      const int key0 = k_begin + t * kKeyTile;
+      nvalid = min(kKeyTile, k_end - key0);
+      const size_t off = (((size_t)b * p.hkv + g) * p.cap + key0) * RB;
+      kb = kc + off;
+      vb = vc + off;
+      stride = RB;
+    } else {
+      nvalid = p.n;
+      const size_t off = ((size_t)b * p.n * p.hkv + g) * RB;
+      kb = kn + off;
+      vb = vn + off;
+      stride = (size_t)p.hkv * RB;
+    }
+    const int slot = lane % CH;
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      const int row0 = (wave * IPW + i) * G_::kKeysPerInst;
+      const int row = row0 + lane / CH;
+      const int src = row < nvalid ? row : nvalid - 1;
+      const size_t goff = src * stride + (size_t)((slot ^ swz<D>(row)) * 16);
+      __builtin_amdgcn_global_load_lds(kb + goff, (lds_void*)(dK + row0 * RB), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vb + goff, (lds_void*)(dV + row0 * RB), 16, 0, 0);
+    }
+  };
+
+  // Start streaming the first tiles before anything else.
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
+  if (0 < n_tiles) issue(0, S0{});
+  if (1 < n_tiles) issue(1, S1{});
+  if (2 < n_tiles) issue(2, S2{});
 
   // ---- ancestor words of the packed tree: anc[i] = {i} u anc[parent(i)].
   if (TREE && has_new && tid < p.n) {
@@ -107,17 +207,19 @@ __global__ __launch_bounds__(kWaves * 64) void attn_bf16_partial(AttnParams p) {
   }
 
   // ---- this wave's query rows, held as MFMA B operands for the whole split.
-  const int tile0 = rg * (kWaves * TPW) + wave * TPW;
   const int n_row_tiles = (p.rows + 15) >> 4;
+  const int tile0 = rg * p.tiles_per_group + wave * TPW;
+  bool act[TPW];
   bf16x8 qf[TPW][KS];
   int node_of[TPW];
 #pragma unroll
   for (int j = 0; j < TPW; ++j) {
+    act[j] = (wave * TPW + j < p.tiles_per_group) && (tile0 + j < n_row_tiles);
     const int row = (tile0 + j) * 16 + lr;
     node_of[j] = p.n;  // padding rows: treated as seeing every key
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qf[j][ks] = bf16x8{};
-    if (row < p.rows) {
+    if (act[j] && row < p.rows) {
       const int node = row / p.group;
       const int hl = row - node * p.group;
       node_of[j] = node;
@@ -139,59 +241,15 @@ __global__ __launch_bounds__(kWaves * 64) void attn_bf16_partial(AttnParams p) {
   }
   const float c = p.scale_log2;
 
-  // ---- global -> register -> LDS staging, double buffered.
-  u32x4 rk[NL], rv[NL];
-  auto fetch = [&](int t) {
-    const __bf16* kb;
-    const __bf16* vb;
-    size_t stride;
-    int nvalid;
-    if (t < n_ctx_tiles) {
-      const int key0 = k_begin + t * kKeyTile;
-      nvalid = min(kKeyTile, k_end - key0);
-      const size_t off = (((size_t)b * p.hkv + g) * p.cap + key0) * D;
-      kb = kc + off;
-      vb = vc + off;
-      stride = D;
-    } else {
-      nvalid = p.n;
-      const size_t off = ((size_t)b * p.n * p.hkv + g) * D;
-      kb = kn + off;
-      vb = vn + off;
-      stride = (size_t)p.hkv * D;
-    }
-#pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      const int cidx = tid + i * kWaves * 64;
-      const int key = cidx / CH;
-      const int col = cidx % CH;
-      if (key < nvalid) {
-        rk[i] = *reinterpret_cast<const u32x4*>(kb + key * stride + col * 8);
-        rv[i] = *reinterpret_cast<const u32x4*>(vb + key * stride + col * 8);
-      } else {  // zero K and V outside the valid keys: P is 0 there and 0 * 0 stays 0
-        rk[i] = u32x4{0u, 0u, 0u, 0u};
-        rv[i] = u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-  };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      const int cidx = tid + i * kWaves * 64;
-      const int key = cidx / CH;
-      const int col = cidx % CH;
-      *reinterpret_cast<u32x4*>(&sK[buf][key * ST + col * 8]) = rk[i];
-      *reinterpret_cast<u32x4*>(&sV[buf][key * ST + col * 8]) = rv[i];
-    }
-  };
-
-  auto compute = [&](int buf, int t) {
+  auto compute = [&](auto stage, int t) {
+    constexpr int st = decltype(stage)::value;
     const bool is_new = (t == n_ctx_tiles);
     const int nvalid = is_new ? p.n : min(kKeyTile, k_end - (k_begin + t * kKeyTile));
-    const __bf16* Kt = sK[buf];
-    const __bf16* Vt = sV[buf];
+    const bool masked = is_new || nvalid < kKeyTile;
+    const char* Kt = st == 0 ? sK0 : st == 1 ? sK1 : st == 2 ? sK2 : sK3;
+    const char* Vt = st == 0 ? sV0 : st == 1 ? sV1 : st == 2 ? sV2 : sV3;
 
-    // S^T = K Q^T for keys 32*kk + 8*lg' + 4*sub + (lane&3), lg' = (lane&15)>>2 on the A side.
+    // S^T = K Q^T for keys 32*kk + 8*(lr>>2) + 4*sub + (lr&3) on the A side.
     f32x4 sc[TPW][2][2];
 #pragma unroll
     for (int j = 0; j < TPW; ++j)
@@ -203,13 +261,15 @@ __global__ __launch_bounds__(kWaves * 64) void attn_bf16_partial(AttnParams p) {
     for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
-        const int krow = 32 * kk + 8 * (lr >> 2) + 4 * sub + (lane & 3);
+        const int krow = 32 * kk + 8 * (lr >> 2) + 4 * sub + (lr & 3);
+        const int ksw = swz<D>(krow);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 kop = as_bf16x8(*reinterpret_cast<const u32x4*>(Kt + krow * ST + 32 * ks + 8 * lg));
+          const bf16x8 kop = as_bf16x8(
+              *reinterpret_cast<const u32x4*>(Kt + krow * RB + ((4 * ks + lg) ^ ksw) * 16));
 #pragma unroll
           for (int j = 0; j < TPW; ++j)
-            if (tile0 + j < n_row_tiles)
+            if (act[j])
               sc[j][kk][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qf[j][ks], sc[j][kk][sub], 0, 0, 0);
         }
       }
@@ -218,29 +278,45 @@ __global__ __launch_bounds__(kWaves * 64) void attn_bf16_partial(AttnParams p) {
     // Mask, online softmax.  Result lane l holds row lr and keys 32*kk + 8*lg + 4*sub + i.
 #pragma unroll
     for (int j = 0; j < TPW; ++j) {
-      unsigned long long anc = ~0ull;
-      if (TREE && is_new && node_of[j] < p.n) anc = sAnc[node_of[j]];
+      if (!act[j]) continue;
+      if (masked) {
+        unsigned long long anc = ~0ull;
+        if (TREE && is_new && node_of[j] < p.n) anc = sAnc[node_of[j]];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int key = 32 * kk + 8 * lg + 4 * sub + i;
+              bool vis = key < nvalid;
+              if (TREE && is_new) vis = vis && ((anc >> key) & 1ull);
+              if (!vis) sc[j][kk][sub][i] = kNegInf;
+            }
+      }
       float mx = kNegInf;
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int key = 32 * kk + 8 * lg + 4 * sub + i;
-            bool vis = key < nvalid;
-            if (TREE && is_new) vis = vis && ((anc >> key) & 1ull);
-            const float v = vis ? sc[j][kk][sub][i] : kNegInf;
-            sc[j][kk][sub][i] = v;
-            mx = fmaxf(mx, v);
-          }
+          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[j][kk][sub][i]);
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[j], mx);
-      const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-      const float alpha = exp2f((m_run[j] - m_use) * c);
-      m_run[j] = m_new;
-      const float neg = -m_use * c;
+      // Lazy rescaling: the reference maximum m_run moves only when a score
+      // exceeds it by more than 2^kSlack in exp2 units, so most tiles skip the
+      // rescale of O.  Probabilities then stay below 2^kSlack, far inside the
+      // fp32 range of the sums and the bf16 range of P.
+      if (__builtin_amdgcn_ballot_w64(mx * c > m_run[j] * c + kSlack || m_run[j] == kNegInf)) {
+        const float m_new = fmaxf(m_run[j], mx);
+        const float m_use = (m_new == kNegInf) ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f((m_run[j] - m_use) * c);
+        m_run[j] = m_use;
+        l_run[j] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[j][dt] *= alpha;
+      }
+      const float neg = -m_run[j] * c;
       float lsum = 0.f;
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
@@ -248,13 +324,12 @@ __global__ __launch_bounds__(kWaves * 64) void attn_bf16_partial(AttnParams p) {
         for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float e = exp2f(fmaf(sc[j][kk][sub][i], c, neg));
+            // argument <= 0; v_exp_f32 flushes the far tail to 0, which is what the sum wants
+            const float e = __builtin_amdgcn_exp2f(fmaf(sc[j][kk][sub][i], c, neg));
             sc[j][kk][sub][i] = e;
             lsum += e;
           }
-      l_run[j] = l_run[j] * alpha + lsum;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o[j][dt] *= alpha;
+      l_run[j] += lsum;
     }
 
     // O^T += V^T P^T.  ds_read_b64_tr_b16: in each 16-lane group, lane jl reads
@@ -272,37 +347,48 @@ __global__ __launch_bounds__(kWaves * 64) void attn_bf16_partial(AttnParams p) {
         }
       }
       const int vrow = 32 * kk + 8 * lg + (lr >> 2);
+      const int vsw_lo = swz<D>(vrow);
+      const int vsw_hi = swz<D>(vrow + 4);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const __bf16* va = Vt + vrow * ST + 16 * dt + 4 * (lane & 3);
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va + 4 * ST));
+        const int chunk = 2 * dt + ((lane & 3) >> 1);
+        const int half = (lane & 1) * 8;
+        const char* va_lo = Vt + vrow * RB + (chunk ^ vsw_lo) * 16 + half;
+        const char* va_hi = Vt + (vrow + 4) * RB + (chunk ^ vsw_hi) * 16 + half;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va_lo));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va_hi));
         // whole-vector reinterpretation: element-wise bf16 inserts of the 16-bit
         // lanes were miscompiled (every element became lo[0])
         const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
         for (int j = 0; j < TPW; ++j)
-          if (tile0 + j < n_row_tiles)
+          if (act[j])
             o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pb[j], o[j][dt], 0, 0, 0);
       }
     }
   };
 
-  fetch(0);
-  stash(0);
-  __syncthreads();
-  for (int t = 0; t < n_tiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < n_tiles) fetch(t + 1);
-    compute(buf, t);
-    if (t + 1 < n_tiles) stash(buf ^ 1);
-    __syncthreads();
+  // Tile t lives in stage t % 4; the loop is unrolled by the ring depth so
+  // that every LDS access names its stage at compile time.
+  auto step = [&](int t, auto cur, auto nxt) {
+    // own loads of tile t done (tiles t+1, t+2 may still be in flight)
+    if (t + kStages - 2 < n_tiles) wait_vmcnt<(kStages - 2) * LOADS_PER_TILE>();
+    else wait_vmcnt<0>();
+    lds_barrier();  // every wave's loads of tile t landed; the stage of tile t-1 is free
+    if (t + kStages - 1 < n_tiles) issue(t + kStages - 1, nxt);
+    compute(cur, t);
+  };
+  for (int t = 0; t < n_tiles; t += kStages) {
+    step(t, S0{}, S3{});
+    if (t + 1 < n_tiles) step(t + 1, S1{}, S0{});
+    if (t + 2 < n_tiles) step(t + 2, S2{}, S1{});
+    if (t + 3 < n_tiles) step(t + 3, S3{}, S2{});
   }
 
   // ---- partial results of this split: O unnormalised, (max * c, sum).
 #pragma unroll
   for (int j = 0; j < TPW; ++j) {
-    if (tile0 + j >= n_row_tiles) continue;
+    if (!act[j]) continue;
     float l = l_run[j];
     l += __shfl_xor(l, 16);
     l += __shfl_xor(l, 32);
@@ -320,17 +406,23 @@ int grid_blocks(const AttnParams& p) {
   return ((groups + 7) / 8) * 8 * p.row_groups;
 }
 
+template <int D, bool TREE>
+void launch_d(const AttnParams& p, hipStream_t s) {
+  const dim3 grid(grid_blocks(p)), block(kBf16Waves * 64);
+  if (p.tiles_per_wave == 2) hipLaunchKernelGGL((attn_bf16_partial<D, TREE, 2>), grid, block, 0, s, p);
+  else hipLaunchKernelGGL((attn_bf16_partial<D, TREE, 1>), grid, block, 0, s, p);
+}
+
 }  // namespace
 
 hipError_t launch_attn_bf16(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  const dim3 grid(grid_blocks(p)), block(kWaves * 64);
   if (ev0) (void)hipEventRecord(ev0, s);
   if (p.d == 128) {
-    if (tree) hipLaunchKernelGGL((attn_bf16_partial<128, true>), grid, block, 0, s, p);
-    else hipLaunchKernelGGL((attn_bf16_partial<128, false>), grid, block, 0, s, p);
+    if (tree) launch_d<128, true>(p, s);
+    else launch_d<128, false>(p, s);
   } else {
-    if (tree) hipLaunchKernelGGL((attn_bf16_partial<64, true>), grid, block, 0, s, p);
-    else hipLaunchKernelGGL((attn_bf16_partial<64, false>), grid, block, 0, s, p);
+    if (tree) launch_d<64, true>(p, s);
+    else launch_d<64, false>(p, s);
   }
   hipError_t e = hipGetLastError();
   if (ev1) (void)hipEventRecord(ev1, s);

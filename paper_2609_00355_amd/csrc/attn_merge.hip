@@ -32,21 +32,44 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   const int nsb = ctx > 0 ? (ctx + p.split_keys - 1) / p.split_keys : 1;
 
   const size_t base = ((size_t)b * p.hkv + g) * p.nsplit * p.rows_pad + r;
+  // pass 1: the largest split maximum, lanes striding over the splits
   float M = -__builtin_inff();
-  for (int s = 0; s < nsb; ++s) M = fmaxf(M, p.part_ml[base + (size_t)s * p.rows_pad].x);
+  for (int s = lane; s < nsb; s += 64) M = fmaxf(M, p.part_ml[base + (size_t)s * p.rows_pad].x);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+  // pass 2: lane s of each 64-split chunk computes the weight of split s; the
+  // weights are broadcast while every lane accumulates its own output dims,
+  // with the partial loads of several splits in flight at once.
   float lsum = 0.f;
   float acc[DPL];
 #pragma unroll
   for (int k = 0; k < DPL; ++k) acc[k] = 0.f;
-  for (int s = 0; s < nsb; ++s) {
-    const size_t pr = base + (size_t)s * p.rows_pad;
-    const float2 ml = p.part_ml[pr];
-    const float w = exp2f(ml.x - M);
-    lsum = fmaf(w, ml.y, lsum);
-    const float* po = p.part_o + pr * D + lane * DPL;
+  for (int s0 = 0; s0 < nsb; s0 += 64) {
+    float w = 0.f;
+    if (s0 + lane < nsb) {
+      const float2 ml = p.part_ml[base + (size_t)(s0 + lane) * p.rows_pad];
+      w = exp2f(ml.x - M);
+      lsum = fmaf(w, ml.y, lsum);
+    }
+    const int cnt = min(64, nsb - s0);
+    for (int k0 = 0; k0 < cnt; k0 += 8) {
+      float wk[8], v[8][DPL];
 #pragma unroll
-    for (int k = 0; k < DPL; ++k) acc[k] = fmaf(w, po[k], acc[k]);
+      for (int u = 0; u < 8; ++u) {
+        const int k = k0 + u;
+        wk[u] = __shfl(w, k & 63);  // 0 past the last split
+        const float* po = p.part_o + (base + (size_t)(s0 + k) * p.rows_pad) * D + lane * DPL;
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) v[u][e] = k < cnt ? po[e] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) acc[e] = fmaf(wk[u], v[u][e], acc[e]);
+    }
   }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) lsum += __shfl_xor(lsum, off);
   const float inv = 1.f / lsum;
   if (BF16) {
     __bf16* out = static_cast<__bf16*>(p.out) + row * D + lane * DPL;

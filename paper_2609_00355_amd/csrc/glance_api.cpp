@@ -5,6 +5,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <string>
@@ -34,10 +35,14 @@ bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Default split size: aim at about four workgroups per compute unit over the
+// Default split size: aim at about two workgroups per compute unit over the
 // whole grid, with at least 256 and at most 8192 context keys per split.
 int auto_split_keys(const glance_attn_shape& s, int row_groups) {
-  const long long target_wgs = 1024;
+  long long target_wgs = 512;
+  if (const char* e = getenv("GLANCE_TARGET_WGS")) {  // tuning override
+    const long long v = atoll(e);
+    if (v >= 8 && v <= (1 << 20)) target_wgs = v;
+  }
   const long long cap = s.ctx_capacity > 0 ? s.ctx_capacity : 1;
   long long per = cap * s.batch * s.n_kv_heads * row_groups / target_wgs;
   per = (per + glance::kKeyTile - 1) / glance::kKeyTile * glance::kKeyTile;
@@ -94,9 +99,26 @@ glance_status make_plan(const glance_attn_shape* s, Plan* out) {
   p.cap = s->ctx_capacity;
   p.d = s->head_dim;
   p.rows = p.n * p.group;
-  const int rb = s->dtype == GLANCE_BF16 ? glance::kBf16RowBlock : glance::kF32RowBlock;
-  p.row_groups = (p.rows + rb - 1) / rb;
-  p.rows_pad = p.row_groups * rb;
+  if (s->dtype == GLANCE_BF16) {
+    // 16-row tiles: one per wave when they all fit in one workgroup, else two
+    // per wave (each K/V operand read from LDS then feeds two MFMAs), spread
+    // evenly over the fewest row groups.
+    const int tiles = (p.rows + 15) / 16;
+    p.tiles_per_wave = tiles <= glance::kBf16Waves ? 1 : glance::kBf16MaxTilesPerWave;
+    if (const char* e = getenv("GLANCE_TILES_PER_WAVE")) {  // tuning override
+      const int v = atoi(e);
+      if (v == 1 || v == 2) p.tiles_per_wave = v;
+    }
+    const int per_group_max = glance::kBf16Waves * p.tiles_per_wave;
+    p.row_groups = (tiles + per_group_max - 1) / per_group_max;
+    p.tiles_per_group = (tiles + p.row_groups - 1) / p.row_groups;
+    p.rows_pad = tiles * 16;
+  } else {
+    p.row_groups = (p.rows + glance::kF32RowBlock - 1) / glance::kF32RowBlock;
+    p.tiles_per_group = 0;
+    p.tiles_per_wave = 0;
+    p.rows_pad = p.row_groups * glance::kF32RowBlock;
+  }
   p.split_keys = s->split_keys > 0 ? s->split_keys : auto_split_keys(*s, p.row_groups);
   p.nsplit = p.cap > 0 ? (p.cap + p.split_keys - 1) / p.split_keys : 1;
   const float scale = s->sm_scale > 0.f ? s->sm_scale : 1.0f / sqrtf((float)s->head_dim);

@@ -13,9 +13,10 @@ constexpr int kWaves = 4;
 // Rows per workgroup of the fp32 attention kernel (kWaves waves x 8 rows).
 constexpr int kF32RowsPerWave = 8;
 constexpr int kF32RowBlock = kWaves * kF32RowsPerWave;
-// Row tiles per wave of the bf16 MFMA kernel (16 rows per tile).
-constexpr int kBf16TilesPerWave = 2;
-constexpr int kBf16RowBlock = kWaves * kBf16TilesPerWave * 16;
+// Waves per workgroup of the bf16 matrix-core kernel (two per SIMD) and the
+// most 16-row tiles one of its waves holds.
+constexpr int kBf16Waves = 8;
+constexpr int kBf16MaxTilesPerWave = 2;
 
 // Everything a split-KV attention launch needs.  Layouts:
 //   q      [batch][n][hq][d]         k_ctx/v_ctx [batch][hkv][cap][d]
@@ -40,7 +41,9 @@ struct AttnParams {
   int batch, n, hq, hkv, group, cap, d;
   int rows;       // n * group
   int rows_pad;   // rows rounded up to the kernel's row block
-  int row_groups; // workgroups sharing one KV split (rows_pad / row block)
+  int row_groups; // workgroups sharing one KV split
+  int tiles_per_group;  // 16-row tiles per row group (bf16 kernel)
+  int tiles_per_wave;   // 16-row tiles per wave, 1 or 2 (bf16 kernel)
   int nsplit;     // split slots per (sequence, KV head) = ceil(cap / split_keys), >= 1
   int split_keys; // context keys per split, multiple of kKeyTile
   float scale_log2;  // sm_scale * log2(e)
