@@ -11,7 +11,10 @@
 // so several tiles are in flight per workgroup while the current one is
 // consumed.  Rows of the tile are stored unpadded with the 16-byte chunks of
 // key k permuted by an XOR with swz(k), which keeps both the K-operand reads
-// and the transposed V reads free of bank conflicts.
+// and the transposed V reads free of bank conflicts.  The loads are issued
+// from inline assembly and waited for explicitly (s_waitcnt vmcnt), because
+// the compiler, seeing a load into LDS in flight, would otherwise wait for
+// all of them before every LDS read and drain the ring.
 //
 // Per tile each wave computes, for each of its 16-row tiles,
 //   S^T[key][row] = K[key][:] . Q[row][:]        (v_mfma_f32_16x16x32_bf16, A = K, B = Q^T)
@@ -60,9 +63,25 @@ struct Geom {
 // neighbouring chunks.  Both land on distinct 16-byte bank groups.
 template <int D>
 __device__ __forceinline__ int swz(int k) {
-  int s = ((k & 3) << 1) | ((k >> 3) & 1);
-  if (D >= 128) s |= (k >> 1) & 8;
-  return s;
+  if (D >= 128) return ((k & 3) << 1) | (((k >> 3) & 1) << 3) | ((k >> 4) & 1);
+  return ((k & 3) << 1) | ((k >> 3) & 1);
+}
+
+// One 16-byte-per-lane load from global memory into LDS: lane i writes LDS
+// bytes [lds_base + 16 i, +16).  M0 carries the wave-uniform LDS base; it is
+// saved and restored around the load (the compiler owns M0), and one wait
+// state separates the M0 write from the load that reads it.
+__device__ __forceinline__ void dma16(const void* gptr, unsigned lds_base) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(gptr)
+      : "memory");
 }
 
 // s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
@@ -95,19 +114,8 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   constexpr int LOADS_PER_TILE = 2 * IPW;  // K and V load instructions per wave per tile
   static_assert(IPW * G_::kKeysPerInst * kBf16Waves == kKeyTile, "tile load must divide evenly");
 
-  // One LDS variable per ring stage and tensor, always addressed with a
-  // compile-time stage index: the compiler can then tell that reading stage A
-  // does not alias the DMA still landing in stage B, and waits only as told.
-  __shared__ __attribute__((aligned(1024))) char sK0[G_::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) char sK1[G_::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) char sK2[G_::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) char sK3[G_::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) char sV0[G_::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) char sV1[G_::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) char sV2[G_::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) char sV3[G_::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char sRing[kStages][2][G_::kTileBytes];
   __shared__ unsigned long long sAnc[64];
-  static_assert(kStages == 4, "one LDS variable per stage");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -149,10 +157,10 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   // [8w, 8w+8); lane i of a load writes LDS row base + i/CH, chunk slot i%CH,
   // which holds global chunk slot ^ swz(row).  Rows past the valid keys re-read
   // the last valid row: their scores are masked, so P = 0 and V is finite.
-  auto issue = [&](int t, auto stage) {
-    constexpr int st = decltype(stage)::value;
-    char* dK = st == 0 ? sK0 : st == 1 ? sK1 : st == 2 ? sK2 : sK3;
-    char* dV = st == 0 ? sV0 : st == 1 ? sV1 : st == 2 ? sV2 : sV3;
+  auto issue = [&](int t) {
+    const int st = t % kStages;
+    const unsigned lk = (unsigned)(size_t)(&sRing[st][0][0]);
+    const unsigned lv = (unsigned)(size_t)(&sRing[st][1][0]);
     const char* kb;
     const char* vb;
     size_t stride;
@@ -178,19 +186,15 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
       const int row = row0 + lane / CH;
       const int src = row < nvalid ? row : nvalid - 1;
       const size_t goff = src * stride + (size_t)((slot ^ swz<D>(row)) * 16);
-      __builtin_amdgcn_global_load_lds(kb + goff, (lds_void*)(dK + row0 * RB), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vb + goff, (lds_void*)(dV + row0 * RB), 16, 0, 0);
+      dma16(kb + goff, lk + row0 * RB);
+      dma16(vb + goff, lv + row0 * RB);
     }
   };
 
   // Start streaming the first tiles before anything else.
-  using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, 1>;
-  using S2 = std::integral_constant<int, 2>;
-  using S3 = std::integral_constant<int, 3>;
-  if (0 < n_tiles) issue(0, S0{});
-  if (1 < n_tiles) issue(1, S1{});
-  if (2 < n_tiles) issue(2, S2{});
+#pragma unroll
+  for (int t = 0; t < kStages - 1; ++t)
+    if (t < n_tiles) issue(t);
 
   // ---- ancestor words of the packed tree: anc[i] = {i} u anc[parent(i)].
   if (TREE && has_new && tid < p.n) {
@@ -209,12 +213,16 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   // ---- this wave's query rows, held as MFMA B operands for the whole split.
   const int n_row_tiles = (p.rows + 15) >> 4;
   const int tile0 = rg * p.tiles_per_group + wave * TPW;
+  // Inactive tiles (past this row group or past the last row) compute on a
+  // zero query and are not written; a wave with none skips the arithmetic.
   bool act[TPW];
   bf16x8 qf[TPW][KS];
   int node_of[TPW];
+  bool wave_active = false;
 #pragma unroll
   for (int j = 0; j < TPW; ++j) {
     act[j] = (wave * TPW + j < p.tiles_per_group) && (tile0 + j < n_row_tiles);
+    wave_active = wave_active || act[j];
     const int row = (tile0 + j) * 16 + lr;
     node_of[j] = p.n;  // padding rows: treated as seeing every key
 #pragma unroll
@@ -241,13 +249,15 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   }
   const float c = p.scale_log2;
 
-  auto compute = [&](auto stage, int t) {
-    constexpr int st = decltype(stage)::value;
+  // MASKED: the tile holds invalid keys (the ragged last context tile) or is
+  // the new-key tile; full context tiles take the unmasked instantiation.
+  auto compute = [&](auto masked_tag, int t) {
+    constexpr bool masked = decltype(masked_tag)::value;
+    const int st = t % kStages;
     const bool is_new = (t == n_ctx_tiles);
     const int nvalid = is_new ? p.n : min(kKeyTile, k_end - (k_begin + t * kKeyTile));
-    const bool masked = is_new || nvalid < kKeyTile;
-    const char* Kt = st == 0 ? sK0 : st == 1 ? sK1 : st == 2 ? sK2 : sK3;
-    const char* Vt = st == 0 ? sV0 : st == 1 ? sV1 : st == 2 ? sV2 : sV3;
+    const char* Kt = sRing[st][0];
+    const char* Vt = sRing[st][1];
 
     // S^T = K Q^T for keys 32*kk + 8*(lr>>2) + 4*sub + (lr&3) on the A side.
     f32x4 sc[TPW][2][2];
@@ -269,8 +279,7 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
               *reinterpret_cast<const u32x4*>(Kt + krow * RB + ((4 * ks + lg) ^ ksw) * 16));
 #pragma unroll
           for (int j = 0; j < TPW; ++j)
-            if (act[j])
-              sc[j][kk][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qf[j][ks], sc[j][kk][sub], 0, 0, 0);
+            sc[j][kk][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qf[j][ks], sc[j][kk][sub], 0, 0, 0);
         }
       }
     }
@@ -278,7 +287,6 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
     // Mask, online softmax.  Result lane l holds row lr and keys 32*kk + 8*lg + 4*sub + i.
 #pragma unroll
     for (int j = 0; j < TPW; ++j) {
-      if (!act[j]) continue;
       if (masked) {
         unsigned long long anc = ~0ull;
         if (TREE && is_new && node_of[j] < p.n) anc = sAnc[node_of[j]];
@@ -362,27 +370,24 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
         const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
         for (int j = 0; j < TPW; ++j)
-          if (act[j])
-            o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pb[j], o[j][dt], 0, 0, 0);
+          o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pb[j], o[j][dt], 0, 0, 0);
       }
     }
   };
 
-  // Tile t lives in stage t % 4; the loop is unrolled by the ring depth so
-  // that every LDS access names its stage at compile time.
-  auto step = [&](int t, auto cur, auto nxt) {
-    // own loads of tile t done (tiles t+1, t+2 may still be in flight)
+  // Tile t lives in ring stage t % kStages.  Full context tiles come first;
+  // the ragged last context tile and the new-key tile (if any) need the mask.
+  const int n_full = (k_end - k_begin) / kKeyTile;
+  for (int t = 0; t < n_tiles; ++t) {
+    // own loads of tile t done (tiles t+1 .. t+kStages-2 may still be in flight)
     if (t + kStages - 2 < n_tiles) wait_vmcnt<(kStages - 2) * LOADS_PER_TILE>();
     else wait_vmcnt<0>();
     lds_barrier();  // every wave's loads of tile t landed; the stage of tile t-1 is free
-    if (t + kStages - 1 < n_tiles) issue(t + kStages - 1, nxt);
-    compute(cur, t);
-  };
-  for (int t = 0; t < n_tiles; t += kStages) {
-    step(t, S0{}, S3{});
-    if (t + 1 < n_tiles) step(t + 1, S1{}, S0{});
-    if (t + 2 < n_tiles) step(t + 2, S2{}, S1{});
-    if (t + 3 < n_tiles) step(t + 3, S3{}, S2{});
+    if (t + kStages - 1 < n_tiles) issue(t + kStages - 1);
+    if (wave_active) {
+      if (t < n_full) compute(std::false_type{}, t);
+      else compute(std::true_type{}, t);
+    }
   }
 
   // ---- partial results of this split: O unnormalised, (max * c, sum).
