@@ -375,6 +375,11 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
     }
   };
 
+  // Let every load the compiler knows about (queries, parents) land now: it
+  // cannot see the tile loads above, so a wait it would place inside the loop
+  // for a first use there (vmcnt(0)) would drain the ring on every iteration.
+  wait_vmcnt<0>();
+
   // Tile t lives in ring stage t % kStages.  Full context tiles come first;
   // the ragged last context tile and the new-key tile (if any) need the mask.
   const int n_full = (k_end - k_begin) / kKeyTile;

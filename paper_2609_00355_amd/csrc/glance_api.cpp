@@ -35,10 +35,10 @@ bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Default split size: aim at about two workgroups per compute unit over the
+// Default split size: aim at about one workgroup per compute unit over the
 // whole grid, with at least 256 and at most 8192 context keys per split.
 int auto_split_keys(const glance_attn_shape& s, int row_groups) {
-  long long target_wgs = 512;
+  long long target_wgs = 256;
   if (const char* e = getenv("GLANCE_TARGET_WGS")) {  // tuning override
     const long long v = atoll(e);
     if (v >= 8 && v <= (1 << 20)) target_wgs = v;
