@@ -43,6 +43,11 @@ def parse():
     ap.add_argument("--graph", action="store_true", help="replay the round from a captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 256 MiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench "
+                         "with --calibrate-copy into profiles/traffic.json, then exit")
     return ap.parse_args()
 
 
@@ -87,6 +92,57 @@ def load_traffic(kernel_key, src):
     return rec.get("bytes_per_launch")
 
 
+COPY_BYTES = 256 << 20
+COPY_KERNEL = "neg_kernel"  # the calibration copy: out = -in over COPY_BYTES of fp32
+KERNEL_KEYS = {"draft": "attn_bf16_partial<128, false", "verify": "attn_bf16_partial<128, true",
+               "accept": "argmax_partial<true, true>"}
+KERNEL_SRC = {"draft": "attn_bf16.hip", "verify": "attn_bf16.hip", "accept": "accept.hip"}
+
+
+def summarise_traffic(fetch_dir, write_dir):
+    """Per-launch HBM bytes of the round's main kernels from rocprofv3 counter CSVs.
+
+    FETCH_SIZE and WRITE_SIZE read KiB per dispatch; each is scaled by the
+    ratio between the bytes a plain streaming kernel over COPY_BYTES really
+    moves (reads COPY_BYTES, writes COPY_BYTES) and what the same counter
+    reports for it.
+    """
+    import csv
+    import glob
+
+    def load(d, counter):
+        per = {}
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] != counter:
+                    continue
+                per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return per
+
+    fetch, write = load(fetch_dir, "FETCH_SIZE"), load(write_dir, "WRITE_SIZE")
+
+    def avg(per, key):
+        vals = [v for k, vs in per.items() if key in k for v in vs]
+        return sum(vals) / len(vals) if vals else None
+
+    f_copy, w_copy = avg(fetch, COPY_KERNEL), avg(write, COPY_KERNEL)
+    if not f_copy or not w_copy:
+        raise SystemExit("no copy-kernel reading in the counter runs (use --calibrate-copy)")
+    f_scale, w_scale = COPY_BYTES / (f_copy * 1024), COPY_BYTES / (w_copy * 1024)
+    out = {"copy_bytes": COPY_BYTES, "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)}
+    for name, key in KERNEL_KEYS.items():
+        f, w = avg(fetch, key), avg(write, key)
+        if f is None or w is None:
+            continue
+        src = os.path.join(ROOT, "paper_2609_00355_amd", "csrc", KERNEL_SRC[name])
+        out[name] = {"kernel": key, "source_sha": source_hash(src),
+                     "fetch_bytes": round(f * 1024 * f_scale), "write_bytes": round(w * 1024 * w_scale),
+                     "bytes_per_launch": round((f * 1024 * f_scale) + (w * 1024 * w_scale))}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    json.dump(out, open(path, "w"), indent=1)
+    print(json.dumps(out))
+
+
 def cpu_baseline(inputs, budget_s):
     """The float64 oracle, as it stands, on a bounded sample of the same round."""
     import numpy as np
@@ -123,6 +179,9 @@ def cpu_baseline(inputs, budget_s):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        summarise_traffic(*args.traffic_from)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}, "
@@ -180,6 +239,14 @@ def main():
                 step(s)
             graphs.append(g)
         torch.cuda.synchronize()
+
+    if args.calibrate_copy:  # reference kernel for the HBM byte counters
+        src_c = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        dst_c = torch.empty_like(src_c)
+        for _ in range(3):
+            torch.neg(src_c, out=dst_c)  # a plain streaming kernel: reads and writes COPY_BYTES
+        torch.cuda.synchronize()
+        del src_c, dst_c
 
     for i in range(args.warmup):
         if graphs:
