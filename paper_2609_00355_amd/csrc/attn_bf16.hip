@@ -309,13 +309,15 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
         for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
           for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[j][kk][sub][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      // Lazy rescaling: the reference maximum m_run moves only when a score
-      // exceeds it by more than 2^kSlack in exp2 units, so most tiles skip the
-      // rescale of O.  Probabilities then stay below 2^kSlack, far inside the
-      // fp32 range of the sums and the bf16 range of P.
+      // Lazy rescaling: the reference maximum m_run (uniform over the four
+      // lanes of a row) moves only when a score exceeds it by more than
+      // 2^kSlack in exp2 units, so most tiles skip both the cross-lane maximum
+      // and the rescale of O.  Probabilities stay below 2^kSlack, far inside
+      // the fp32 range of the sums and the bf16 range of P.  The test runs on
+      // each lane's own maximum: no lane above the reference means no row is.
       if (__builtin_amdgcn_ballot_w64(mx * c > m_run[j] * c + kSlack || m_run[j] == kNegInf)) {
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
         const float m_new = fmaxf(m_run[j], mx);
         const float m_use = (m_new == kNegInf) ? 0.f : m_new;
         const float alpha = __builtin_amdgcn_exp2f((m_run[j] - m_use) * c);
