@@ -208,7 +208,11 @@ def main():
     ctx = inputs["ctx_lens"]
     stream = torch.cuda.current_stream()
 
-    # ---- device copies of the input set, outputs and prepared calls
+    # ---- device copies of the input set, outputs and prepared calls.  With
+    # --graph the calls are bound to a side stream that the capture runs on.
+    if args.graph:
+        stream = torch.cuda.Stream()
+        torch.cuda.set_stream(stream)
     sets = []
     for r in range(args.sets):
         dd = {k: t.to(dev) for k, t in inputs["draft"].items()}
@@ -235,7 +239,7 @@ def main():
         graphs = []
         for s in sets:
             g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
+            with torch.cuda.graph(g, stream=stream):
                 step(s)
             graphs.append(g)
         torch.cuda.synchronize()

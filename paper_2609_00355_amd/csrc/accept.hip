@@ -48,6 +48,71 @@ __device__ __forceinline__ unsigned long long wave_max64(unsigned long long v) {
   return v;
 }
 
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+
+// Order keys of the two bf16 values packed in w, as int16 lanes, with packed
+// 16-bit instructions: sign-magnitude -> two's complement, so +0 and -0 both
+// give 0 and every non-NaN value keeps its order.  A NaN gives a key above
+// +inf (0x7f80) or below -inf (-0x7f80); such chunks take the exact scalar path.
+__device__ __forceinline__ s16x2 key2(unsigned w) {
+  const s16x2 x = __builtin_bit_cast(s16x2, w);
+  const s16x2 t = x >> (s16x2){15, 15};                       // -1 for negatives, else 0
+  const s16x2 k = x ^ (t & (s16x2){0x7fff, 0x7fff});          // negatives -> -1 - magnitude
+  return k - t;                                               // negatives -> -magnitude
+}
+
+// bf16 rows with 16-byte alignment: per 8 values, the packed keys are reduced
+// to one maximum, compared once with the thread's running best, and only the
+// position of the 8-value vector that first reached the best is kept.  At the
+// end the thread re-reads that one vector to find the lowest index holding
+// the best key.  Chunks containing a NaN are redone by the exact scalar scan.
+__device__ __forceinline__ void argmax_bf16_fast(const unsigned short* x, int c0, int c1, int tid,
+                                                 int& best_key, int& best_idx) {
+  constexpr int kUnroll = 4;
+  int bk = -0x8000 - 1;  // below every int16 key
+  int bpos = -1;
+  s16x2 lo = (s16x2){0x7fff, 0x7fff};
+  s16x2 hi = (s16x2){-0x7fff, -0x7fff};
+  for (int e0 = c0 + 8 * tid; e0 < c1; e0 += 8 * 256 * kUnroll) {
+    u32x4 v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int e = e0 + u * 8 * 256;
+      v[u] = e < c1 ? *reinterpret_cast<const u32x4*>(x + e) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int e = e0 + u * 8 * 256;
+      if (e >= c1) break;
+      const s16x2 k0 = key2(v[u][0]), k1 = key2(v[u][1]), k2 = key2(v[u][2]), k3 = key2(v[u][3]);
+      const s16x2 mx = __builtin_elementwise_max(__builtin_elementwise_max(k0, k1), __builtin_elementwise_max(k2, k3));
+      const s16x2 mn = __builtin_elementwise_min(__builtin_elementwise_min(k0, k1), __builtin_elementwise_min(k2, k3));
+      hi = __builtin_elementwise_max(hi, mx);
+      lo = __builtin_elementwise_min(lo, mn);
+      const int vm = max((int)mx[0], (int)mx[1]);
+      if (vm > bk) { bk = vm; bpos = e; }
+    }
+  }
+  const bool nan_seen = max((int)hi[0], (int)hi[1]) > 0x7f80 || min((int)lo[0], (int)lo[1]) < -0x7f80;
+  if (__syncthreads_or(nan_seen)) {  // exact path: NaN is the largest value, the first one wins
+    for (int e = c0 + tid; e < c1; e += 256) {
+      const int k = order_key((unsigned int)x[e] << 16);
+      if (k > best_key) { best_key = k; best_idx = e; }
+    }
+    return;
+  }
+  if (bpos >= 0) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(x + bpos);
+#pragma unroll
+    for (int w = 3; w >= 0; --w) {  // backwards, so the lowest index overwrites last
+      const s16x2 k = key2(v[w]);
+      if (k[1] == bk) best_idx = bpos + 2 * w + 1;
+      if (k[0] == bk) best_idx = bpos + 2 * w;
+    }
+    best_key = order_key((unsigned int)x[best_idx] << 16);
+  }
+}
+
 template <bool BF16, bool VEC>
 __global__ __launch_bounds__(256) void argmax_partial(AcceptParams p) {
   __shared__ unsigned long long red[4];
@@ -61,16 +126,7 @@ __global__ __launch_bounds__(256) void argmax_partial(AcceptParams p) {
   if (BF16) {
     const unsigned short* x = static_cast<const unsigned short*>(p.logits) + row * (long)p.vocab;
     if (VEC) {
-      for (int e = c0 + 8 * tid; e < c1; e += 8 * 256) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(x + e);
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const int k0 = order_key(v[w] << 16);
-          const int k1 = order_key(v[w] & 0xffff0000u);
-          if (k0 > best_key) { best_key = k0; best_idx = e + 2 * w; }
-          if (k1 > best_key) { best_key = k1; best_idx = e + 2 * w + 1; }
-        }
-      }
+      argmax_bf16_fast(x, c0, c1, tid, best_key, best_idx);
     } else {
       for (int e = c0 + tid; e < c1; e += 256) {
         const int k = order_key((unsigned int)x[e] << 16);
@@ -80,12 +136,23 @@ __global__ __launch_bounds__(256) void argmax_partial(AcceptParams p) {
   } else {
     const unsigned int* x = static_cast<const unsigned int*>(p.logits) + row * (long)p.vocab;
     if (VEC) {
-      for (int e = c0 + 4 * tid; e < c1; e += 4 * 256) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(x + e);
+      constexpr int kUnroll = 4;
+      for (int e0 = c0 + 4 * tid; e0 < c1; e0 += 4 * 256 * kUnroll) {
+        u32x4 v[kUnroll];
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const int k = order_key(v[w]);
-          if (k > best_key) { best_key = k; best_idx = e + w; }
+        for (int u = 0; u < kUnroll; ++u) {
+          const int e = e0 + u * 4 * 256;
+          v[u] = e < c1 ? *reinterpret_cast<const u32x4*>(x + e) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const int e = e0 + u * 4 * 256;
+          if (e >= c1) break;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const int k = order_key(v[u][w]);
+            if (k > best_key) { best_key = k; best_idx = e + w; }
+          }
         }
       }
     } else {

@@ -209,9 +209,14 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
   if (vocab < 1 || vocab > (1 << 30)) return fail(GLANCE_ERR_INVALID_ARG, "vocab must be in 1..2^30");
   const long long rows = (long long)batch * n_nodes;
   if (rows * (long long)vocab > (1LL << 40)) return fail(GLANCE_ERR_UNSUPPORTED, "logits too large");
-  // about 2048 workgroups over the grid, chunks of at least 4096 values
-  long long chunks = (2048 + rows - 1) / rows;
-  long long max_chunks = ((long long)vocab + 4095) / 4096;
+  // about 512 workgroups over the grid (two per CU), chunks of at least 8192 values
+  long long target = 512;
+  if (const char* e = getenv("GLANCE_ACCEPT_WGS")) {  // tuning override
+    const long long v = atoll(e);
+    if (v >= 1 && v <= (1 << 20)) target = v;
+  }
+  long long chunks = (target + rows - 1) / rows;
+  long long max_chunks = ((long long)vocab + 8191) / 8192;
   if (chunks > max_chunks) chunks = max_chunks;
   if (chunks < 1) chunks = 1;
   long long len = ((long long)vocab + chunks - 1) / chunks;
