@@ -179,13 +179,18 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
       vb = vn + off;
       stride = (size_t)p.hkv * RB;
     }
-    const int slot = lane % CH;
+    // The lane's offsets are recomputed from a laundered lane id each time:
+    // hoisted out of the loop they would stay live across it and push the
+    // kernel into spilling (whose reloads wait for every tile load in flight).
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const unsigned st32 = (unsigned)stride;
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
       const int row0 = (wave * IPW + i) * G_::kKeysPerInst;
-      const int row = row0 + lane / CH;
+      const int row = row0 + ln / CH;
       const int src = row < nvalid ? row : nvalid - 1;
-      const size_t goff = src * stride + (size_t)((slot ^ swz<D>(row)) * 16);
+      const unsigned goff = (unsigned)src * st32 + (unsigned)(((ln % CH) ^ swz<D>(row)) * 16);
       dma16(kb + goff, lk + row0 * RB);
       dma16(vb + goff, lv + row0 * RB);
     }
@@ -196,18 +201,16 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   for (int t = 0; t < kStages - 1; ++t)
     if (t < n_tiles) issue(t);
 
-  // ---- ancestor words of the packed tree: anc[i] = {i} u anc[parent(i)].
-  if (TREE && has_new && tid < p.n) {
-    const int32_t* par = p.parents + (size_t)b * p.n;
-    unsigned long long a = 1ull << tid;
-    int cur = tid;
-    int c = par[tid];
-    for (int step = 0; step < 64 && c >= 0 && c < cur; ++step) {
-      a |= 1ull << c;
-      cur = c;
-      c = par[c];
-    }
-    sAnc[tid] = a;
+  // ---- ancestor words of the packed tree, anc[i] = {i} u anc[parent(i)], by
+  // pointer doubling in wave 0 (one load per node instead of a chain of
+  // dependent loads): after r rounds lane i holds the nodes on its root path
+  // from i up to (excluding) its 2^r-th ancestor up[i].
+  unsigned long long anc_word = 0;
+  int up = -1;
+  if (TREE && has_new && wave == 0 && lane < p.n) {
+    const int par = p.parents[(size_t)b * p.n + lane];
+    up = (par >= 0 && par < lane) ? par : -1;
+    anc_word = 1ull << lane;
   }
 
   // ---- this wave's query rows, held as MFMA B operands for the whole split.
@@ -267,16 +270,16 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub) sc[j][kk][sub] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // k-steps outermost, so that consecutive MFMAs use different accumulators
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+    for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-        const int krow = 32 * kk + 8 * (lr >> 2) + 4 * sub + (lr & 3);
-        const int ksw = swz<D>(krow);
+      for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
+        for (int sub = 0; sub < 2; ++sub) {
+          const int krow = 32 * kk + 8 * (lr >> 2) + 4 * sub + (lr & 3);
           const bf16x8 kop = as_bf16x8(
-              *reinterpret_cast<const u32x4*>(Kt + krow * RB + ((4 * ks + lg) ^ ksw) * 16));
+              *reinterpret_cast<const u32x4*>(Kt + krow * RB + ((4 * ks + lg) ^ swz<D>(krow)) * 16));
 #pragma unroll
           for (int j = 0; j < TPW; ++j)
             sc[j][kk][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qf[j][ks], sc[j][kk][sub], 0, 0, 0);
@@ -315,7 +318,7 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
       // and the rescale of O.  Probabilities stay below 2^kSlack, far inside
       // the fp32 range of the sums and the bf16 range of P.  The test runs on
       // each lane's own maximum: no lane above the reference means no row is.
-      if (__builtin_amdgcn_ballot_w64(mx * c > m_run[j] * c + kSlack || m_run[j] == kNegInf)) {
+      if (__builtin_amdgcn_ballot_w64((mx * c > m_run[j] * c + kSlack) | (m_run[j] == kNegInf))) {
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
         const float m_new = fmaxf(m_run[j], mx);
@@ -381,6 +384,21 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   // cannot see the tile loads above, so a wait it would place inside the loop
   // for a first use there (vmcnt(0)) would drain the ring on every iteration.
   wait_vmcnt<0>();
+
+  if (TREE && has_new && wave == 0) {
+#pragma unroll
+    for (int r = 0; r < 6; ++r) {
+      const int src = up < 0 ? lane : up;
+      const unsigned lo = __shfl((unsigned)anc_word, src);
+      const unsigned hi = __shfl((unsigned)(anc_word >> 32), src);
+      const int up2 = __shfl(up, src);
+      if (up >= 0) {
+        anc_word |= ((unsigned long long)hi << 32) | lo;
+        up = up2;
+      }
+    }
+    if (lane < p.n) sAnc[lane] = anc_word;  // read after the loop's barriers
+  }
 
   // Tile t lives in ring stage t % kStages.  Full context tiles come first;
   // the ragged last context tile and the new-key tile (if any) need the mask.
