@@ -48,69 +48,66 @@ __device__ __forceinline__ unsigned long long wave_max64(unsigned long long v) {
   return v;
 }
 
-typedef short s16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float as_f32(unsigned u) { return __builtin_bit_cast(float, u); }
 
-// Order keys of the two bf16 values packed in w, as int16 lanes, with packed
-// 16-bit instructions: sign-magnitude -> two's complement, so +0 and -0 both
-// give 0 and every non-NaN value keeps its order.  A NaN gives a key above
-// +inf (0x7f80) or below -inf (-0x7f80); such chunks take the exact scalar path.
-__device__ __forceinline__ s16x2 key2(unsigned w) {
-  const s16x2 x = __builtin_bit_cast(s16x2, w);
-  const s16x2 t = x >> (s16x2){15, 15};                       // -1 for negatives, else 0
-  const s16x2 k = x ^ (t & (s16x2){0x7fff, 0x7fff});          // negatives -> -1 - magnitude
-  return k - t;                                               // negatives -> -magnitude
-}
+// IEEE 754-2019 maximum (v_maximum3_f32): a NaN operand gives NaN, and -0 < +0.
+__device__ __forceinline__ float fmaximum(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float fmaximum3(float a, float b, float c) { return fmaximum(fmaximum(a, b), c); }
 
-// bf16 rows with 16-byte alignment: per 8 values, the packed keys are reduced
-// to one maximum, compared once with the thread's running best, and only the
-// position of the 8-value vector that first reached the best is kept.  At the
-// end the thread re-reads that one vector to find the lowest index holding
-// the best key.  Chunks containing a NaN are redone by the exact scalar scan.
+// bf16 rows with 16-byte alignment.  A 32-bit word w holds two bf16 values:
+// the high one read as fp32 is w itself (the low value only adds mantissa
+// bits below the bf16 precision, so the order of distinct bf16 values is
+// kept), the low one is w << 16.  Per 8 values the thread takes one fp32
+// maximum, masks it back to bf16 precision and keeps the first 8-value vector
+// that reached its running best, together with that vector itself, so the
+// lowest index holding the best value is found at the end without a second
+// read.  The maximum propagates NaN, so a chunk holding a NaN (or an infinity,
+// which the extra mantissa bits can turn into a NaN) shows up as a NaN running
+// maximum; such chunks, and chunks whose best value is +0 or -0 (which must
+// tie), are redone by the exact scalar scan.
 __device__ __forceinline__ void argmax_bf16_fast(const unsigned short* x, int c0, int c1, int tid,
                                                  int& best_key, int& best_idx) {
-  constexpr int kUnroll = 4;
-  int bk = -0x8000 - 1;  // below every int16 key
+  constexpr int kUnroll = 8;
+  constexpr unsigned kPad = 0xff7fff7fu;  // two finite -3.39e38 values, never selected
+  float bk = -__builtin_inff();
+  float run = -__builtin_inff();
   int bpos = -1;
-  s16x2 lo = (s16x2){0x7fff, 0x7fff};
-  s16x2 hi = (s16x2){-0x7fff, -0x7fff};
+  u32x4 bv = {0u, 0u, 0u, 0u};
   for (int e0 = c0 + 8 * tid; e0 < c1; e0 += 8 * 256 * kUnroll) {
     u32x4 v[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int e = e0 + u * 8 * 256;
-      v[u] = e < c1 ? *reinterpret_cast<const u32x4*>(x + e) : u32x4{0u, 0u, 0u, 0u};
+      v[u] = e < c1 ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(x + e))
+                    : u32x4{kPad, kPad, kPad, kPad};
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int e = e0 + u * 8 * 256;
-      if (e >= c1) break;
-      const s16x2 k0 = key2(v[u][0]), k1 = key2(v[u][1]), k2 = key2(v[u][2]), k3 = key2(v[u][3]);
-      const s16x2 mx = __builtin_elementwise_max(__builtin_elementwise_max(k0, k1), __builtin_elementwise_max(k2, k3));
-      const s16x2 mn = __builtin_elementwise_min(__builtin_elementwise_min(k0, k1), __builtin_elementwise_min(k2, k3));
-      hi = __builtin_elementwise_max(hi, mx);
-      lo = __builtin_elementwise_min(lo, mn);
-      const int vm = max((int)mx[0], (int)mx[1]);
-      if (vm > bk) { bk = vm; bpos = e; }
+      const float a = fmaximum3(as_f32(v[u][0]), as_f32(v[u][1]), as_f32(v[u][2]));
+      const float b = fmaximum3(as_f32(v[u][3]), as_f32(v[u][0] << 16), as_f32(v[u][1] << 16));
+      const float m = fmaximum3(as_f32(v[u][2] << 16), as_f32(v[u][3] << 16), fmaximum(a, b));
+      run = fmaximum(run, m);
+      const float vm = as_f32(__builtin_bit_cast(unsigned, m) & 0xffff0000u);
+      if ((vm > bk || bpos < 0) && e < c1) { bk = vm; bpos = e; bv = v[u]; }
     }
   }
-  const bool nan_seen = max((int)hi[0], (int)hi[1]) > 0x7f80 || min((int)lo[0], (int)lo[1]) < -0x7f80;
-  if (__syncthreads_or(nan_seen)) {  // exact path: NaN is the largest value, the first one wins
+  const bool redo = run != run || bk == 0.f;
+  if (__syncthreads_or(redo)) {  // exact path: NaN is the largest value, the first one wins
     for (int e = c0 + tid; e < c1; e += 256) {
       const int k = order_key((unsigned int)x[e] << 16);
       if (k > best_key) { best_key = k; best_idx = e; }
     }
     return;
   }
-  if (bpos >= 0) {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(x + bpos);
+  if (bpos < 0) return;
+  unsigned bits = 0;
 #pragma unroll
-    for (int w = 3; w >= 0; --w) {  // backwards, so the lowest index overwrites last
-      const s16x2 k = key2(v[w]);
-      if (k[1] == bk) best_idx = bpos + 2 * w + 1;
-      if (k[0] == bk) best_idx = bpos + 2 * w;
-    }
-    best_key = order_key((unsigned int)x[best_idx] << 16);
+  for (int w = 3; w >= 0; --w) {  // backwards, so the lowest index overwrites last
+    if (as_f32(bv[w] & 0xffff0000u) == bk) { best_idx = bpos + 2 * w + 1; bits = bv[w] >> 16; }
+    if (as_f32(bv[w] << 16) == bk) { best_idx = bpos + 2 * w; bits = bv[w] & 0xffffu; }
   }
+  best_key = order_key(bits << 16);
 }
 
 template <bool BF16, bool VEC>

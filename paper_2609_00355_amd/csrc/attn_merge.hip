@@ -4,26 +4,38 @@
 // maximum of the scaled scores in log2 units, l_s = sum exp2(score - m_s) and
 // O_s = sum exp2(score - m_s) v (unnormalised).  With M = max_s m_s:
 //   out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,   lse = (M + log2 L) ln 2
-// One wave per output row; the row index is the output's own
-// (b, new row, query head) index, so writes are contiguous.
+// D/4 lanes serve one output row, four dims (16 bytes) each, so a wave merges
+// 64/(D/4) rows.  The row index is the output's own (b, new row, query head)
+// index, so writes are contiguous.  The (m, l) pairs and the O partials of up
+// to kChunk splits are loaded together, before any of them is needed, so a row
+// with at most kChunk splits costs one memory round trip; longer rows take
+// further chunks, rescaled online like the attention itself.
 #include "glance_internal.h"
 
 namespace glance {
 namespace {
 
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kMergeWaves = 2;
 
 template <int D, bool BF16>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
-  constexpr int DPL = D / 64;
+__global__ __launch_bounds__(64 * kMergeWaves) void attn_merge_kernel(AttnParams p) {
+  constexpr int LPR = D / 4;     // lanes per row
+  constexpr int RPW = 64 / LPR;  // rows per wave
+  constexpr int kChunk = 16;     // splits in flight per lane
+  static_assert(kChunk <= LPR, "one (m, l) pair per lane and chunk");
   const int lane = threadIdx.x & 63;
-  const long row = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const long total = (long)p.batch * p.n * p.hq;
-  if (row >= total) return;
-  const int h = (int)(row % p.hq);
-  const long bi = row / p.hq;
-  const int i = (int)(bi % p.n);
-  const int b = (int)(bi / p.n);
+  const int q = lane % LPR;
+  const int lead = lane - q;  // first lane of this row
+  // row counts are far below 2^31 (batch * new rows * query heads), so 32-bit index math
+  const int total = p.batch * p.n * p.hq;
+  const int row_raw = ((int)blockIdx.x * kMergeWaves + (int)(threadIdx.x >> 6)) * RPW + lane / LPR;
+  const bool live = row_raw < total;
+  const int row = live ? row_raw : total - 1;  // dead lanes shadow the last row, store nothing
+  const int h = (unsigned)row % (unsigned)p.hq;
+  const int bi = (unsigned)row / (unsigned)p.hq;
+  const int i = (unsigned)bi % (unsigned)p.n;
+  const int b = (unsigned)bi / (unsigned)p.n;
   const int g = h / p.group;
   const int r = i * p.group + (h - g * p.group);
 
@@ -32,62 +44,60 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   const int nsb = ctx > 0 ? (ctx + p.split_keys - 1) / p.split_keys : 1;
 
   const size_t base = ((size_t)b * p.hkv + g) * p.nsplit * p.rows_pad + r;
-  // pass 1: the largest split maximum, lanes striding over the splits
+  const float4* po = reinterpret_cast<const float4*>(p.part_o) + base * (D / 4) + q;
+  const size_t sstride = (size_t)p.rows_pad * (D / 4);  // float4s from one split to the next
+
   float M = -__builtin_inff();
-  for (int s = lane; s < nsb; s += 64) M = fmaxf(M, p.part_ml[base + (size_t)s * p.rows_pad].x);
+  float lsum = 0.f;  // this lane's share of the denominator
+  float4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < nsb; s0 += kChunk) {
+    const int cnt = min(kChunk, nsb - s0);
+    float2 ml = {-__builtin_inff(), 0.f};
+    if (q < cnt) ml = p.part_ml[base + (size_t)(s0 + q) * p.rows_pad];
+    float4 v[kChunk];
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
-  // pass 2: lane s of each 64-split chunk computes the weight of split s; the
-  // weights are broadcast while every lane accumulates its own output dims,
-  // with the partial loads of several splits in flight at once.
-  float lsum = 0.f;
-  float acc[DPL];
+    for (int u = 0; u < kChunk; ++u)
+      v[u] = u < cnt ? po[(size_t)(s0 + u) * sstride] : float4{0.f, 0.f, 0.f, 0.f};
+    float mc = ml.x;
 #pragma unroll
-  for (int k = 0; k < DPL; ++k) acc[k] = 0.f;
-  for (int s0 = 0; s0 < nsb; s0 += 64) {
-    float w = 0.f;
-    if (s0 + lane < nsb) {
-      const float2 ml = p.part_ml[base + (size_t)(s0 + lane) * p.rows_pad];
-      w = exp2f(ml.x - M);
-      lsum = fmaf(w, ml.y, lsum);
+    for (int off = LPR / 2; off >= 1; off >>= 1) mc = fmaxf(mc, __shfl_xor(mc, off));
+    const float Mn = fmaxf(M, mc);
+    const float sc = M == -__builtin_inff() ? 0.f : exp2f(M - Mn);
+    const float w = q < cnt ? exp2f(ml.x - Mn) : 0.f;
+    lsum = fmaf(w, ml.y, lsum * sc);
+    acc.x *= sc; acc.y *= sc; acc.z *= sc; acc.w *= sc;
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) {
+      const float wu = __shfl(w, lead + u);  // 0 past the last split
+      acc.x = fmaf(wu, v[u].x, acc.x);
+      acc.y = fmaf(wu, v[u].y, acc.y);
+      acc.z = fmaf(wu, v[u].z, acc.z);
+      acc.w = fmaf(wu, v[u].w, acc.w);
     }
-    const int cnt = min(64, nsb - s0);
-    for (int k0 = 0; k0 < cnt; k0 += 8) {
-      float wk[8], v[8][DPL];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int k = k0 + u;
-        wk[u] = __shfl(w, k & 63);  // 0 past the last split
-        const float* po = p.part_o + (base + (size_t)(s0 + k) * p.rows_pad) * D + lane * DPL;
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) v[u][e] = k < cnt ? po[e] : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) acc[e] = fmaf(wk[u], v[u][e], acc[e]);
-    }
+    M = Mn;
   }
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) lsum += __shfl_xor(lsum, off);
+  for (int off = LPR / 2; off >= 1; off >>= 1) lsum += __shfl_xor(lsum, off);
+  if (!live) return;
   const float inv = 1.f / lsum;
   if (BF16) {
-    __bf16* out = static_cast<__bf16*>(p.out) + row * D + lane * DPL;
-#pragma unroll
-    for (int k = 0; k < DPL; ++k) out[k] = (__bf16)(acc[k] * inv);
+    typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+    const bf16x4 o = {(__bf16)(acc.x * inv), (__bf16)(acc.y * inv), (__bf16)(acc.z * inv),
+                      (__bf16)(acc.w * inv)};
+    *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(p.out) + (size_t)row * D + 4 * q) = o;
   } else {
-    float* out = static_cast<float*>(p.out) + row * D + lane * DPL;
-#pragma unroll
-    for (int k = 0; k < DPL; ++k) out[k] = acc[k] * inv;
+    *reinterpret_cast<float4*>(static_cast<float*>(p.out) + (size_t)row * D + 4 * q) =
+        float4{acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv};
   }
-  if (p.lse && lane == 0) p.lse[row] = (M + log2f(lsum)) * kLn2;
+  if (p.lse && q == 0) p.lse[row] = (M + log2f(lsum)) * kLn2;
 }
 
 }  // namespace
 
 hipError_t launch_attn_merge(const AttnParams& p, bool out_bf16, hipStream_t s) {
   const long total = (long)p.batch * p.n * p.hq;
-  const dim3 grid((unsigned)((total + 3) / 4)), block(256);
+  const long rows_per_wg = (long)kMergeWaves * 64 / (p.d / 4);
+  const dim3 grid((unsigned)((total + rows_per_wg - 1) / rows_per_wg)), block(64 * kMergeWaves);
   if (p.d == 128) {
     if (out_bf16) hipLaunchKernelGGL((attn_merge_kernel<128, true>), grid, block, 0, s, p);
     else hipLaunchKernelGGL((attn_merge_kernel<128, false>), grid, block, 0, s, p);

@@ -99,6 +99,64 @@ def test_signed_zero_and_nan_semantics():
         assert got["accept_len"].tolist() == [2]
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_special_values_in_long_rows(dtype):
+    """Signed zeros, NaNs, constant rows and a maximum in the last vector of a
+    152064-wide row: the vectorised scan must hand every one of these to the
+    same answer as the plain definition."""
+    vocab = 152064
+    g = torch.Generator().manual_seed(77)
+    x = torch.full((1, 12, vocab), -2.0)
+    x[0, 0, 100000] = -0.0
+    x[0, 0, 120000] = 0.0             # -0 ties with the later +0: 100000
+    x[0, 1, 90000] = -0.0             # -0 alone is the maximum: 90000
+    x[0, 2] = 0.0                     # constant +0: 0
+    x[0, 3] = -float("inf")           # constant -inf: 0
+    x[0, 4, 151000] = float("nan")
+    x[0, 4, 150000] = -float("nan")   # first NaN of either sign: 150000
+    x[0, 5] = torch.randn(vocab, generator=g)
+    x[0, 5, vocab - 1] = 50.0         # maximum in the row's last element: vocab - 1
+    x[0, 6] = 1.5                     # constant: 0
+    x[0, 7] = torch.randn(vocab, generator=g)
+    x[0, 7, 8007] = 50.0
+    x[0, 7, 8008] = 50.0              # tie across a chunk boundary of this 12-row shape: 8007
+    x[0, 8] = torch.randn(vocab, generator=g)
+    x[0, 8, 16383] = x[0, 8, 16384] = x[0, 8, 40000] = 30.0   # 16383
+    x[0, 9] = torch.randn(vocab, generator=g)
+    x[0, 9, 130000] = float("inf")
+    x[0, 9, 123457] = float("inf")    # first +inf: 123457
+    x[0, 10] = -float("inf")
+    x[0, 10, 99999] = -5.0            # the one finite value: 99999
+    x[0, 11, 5000] = 2e-40
+    x[0, 11, 70000] = 3e-40           # subnormal maximum: 70000
+    want = [100000, 90000, 0, 0, 150000, vocab - 1, 0, 8007, 16383, 123457, 99999, 70000]
+    x = x[:, : len(want)]
+    par = torch.arange(-1, len(want) - 1, dtype=torch.int32)[None]
+    tok = torch.tensor([want[:1] + want[:-1]], dtype=torch.int32)
+    logits = x.to(dtype)
+    got = run_accept(logits, par, tok, path_stride=16)
+    assert got["argmax"].tolist() == [want]
+    assert_accept_equal(got, logits, par, tok, path_stride=16)
+
+
+@pytest.mark.parametrize("vocab", [8, 2048, 16384, 16392, 32768 + 8, 65536 + 2048])
+def test_vector_scan_group_boundaries(vocab):
+    """bf16 rows whose lengths sit on and next to the scan's 8-value vector and
+    its 16384-value unrolled step, with the maximum planted in the last element and, in a second
+    row, ties at the first and last element."""
+    g = torch.Generator().manual_seed(vocab)
+    x = torch.randn((2, 3, vocab), generator=g)
+    x[:, 0, vocab - 1] = 40.0
+    x[:, 1, 0] = 40.0
+    x[:, 1, vocab - 1] = 40.0
+    logits = x.to(torch.bfloat16)
+    par = torch.tensor([[-1, 0, 1], [-1, 0, 0]], dtype=torch.int32)
+    tok = torch.tensor([[5, vocab - 1, 0], [5, 0, 1]], dtype=torch.int32)
+    got = run_accept(logits, par, tok)
+    assert got["argmax"][:, :2].tolist() == [[vocab - 1, 0], [vocab - 1, 0]]
+    assert_accept_equal(got, logits, par, tok)
+
+
 def test_path_stride_truncates_but_counts():
     n = 20
     par = torch.arange(-1, n - 1, dtype=torch.int32)[None]
