@@ -84,6 +84,21 @@ __device__ __forceinline__ void dma16(const void* gptr, unsigned lds_base) {
       : "memory");
 }
 
+// The same load with a wave-uniform 64-bit base in SGPRs and a 32-bit
+// per-lane byte offset: no per-lane address arithmetic at issue.
+__device__ __forceinline__ void dma16s(const void* sbase, unsigned voff, unsigned lds_base) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(voff), "s"(sbase)
+      : "memory");
+}
+
 // s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -112,6 +127,7 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   constexpr int CH = G_::kChunks;
   constexpr int IPW = G_::kInstPerWave;
   constexpr int LOADS_PER_TILE = 2 * IPW;  // K and V load instructions per wave per tile
+  constexpr int kAhead = kStages - 1;  // tiles streaming behind the current one
   static_assert(IPW * G_::kKeysPerInst * kBf16Waves == kKeyTile, "tile load must divide evenly");
 
   __shared__ __attribute__((aligned(1024))) char sRing[kStages][2][G_::kTileBytes];
@@ -146,6 +162,9 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   const bool has_new = (s == nsb - 1);
   const int n_ctx_tiles = k_end > k_begin ? (k_end - k_begin + kKeyTile - 1) / kKeyTile : 0;
   const int n_tiles = n_ctx_tiles + (has_new ? 1 : 0);
+  // Full context tiles come first; the ragged last context tile and the
+  // new-key tile (if any) need the mask.
+  const int n_full = (k_end - k_begin) / kKeyTile;
 
   const __bf16* q = static_cast<const __bf16*>(p.q);
   const char* kc = static_cast<const char*>(p.k_ctx);
@@ -153,30 +172,46 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   const char* kn = static_cast<const char*>(p.k_new);
   const char* vn = static_cast<const char*>(p.v_new);
 
-  // ---- issue the loads of tile t into ring stage st.  Wave w fills rows
+  // ---- the loads of tile t into ring stage st.  Wave w fills rows
   // [8w, 8w+8); lane i of a load writes LDS row base + i/CH, chunk slot i%CH,
   // which holds global chunk slot ^ swz(row).  Rows past the valid keys re-read
   // the last valid row: their scores are masked, so P = 0 and V is finite.
-  auto issue = [&](int t) {
+  // A wave's share is LOADS_PER_TILE instructions; issue_part(t, w, q) issues
+  // share q of wave slot w, the K rows (q even) or the V rows (q odd) of its
+  // block q / 2.
+  // Lane offsets of the wave's shares within a full context tile (all 64 rows
+  // valid, row stride RB), computed once; other tiles compute theirs at issue.
+  unsigned full_off[LOADS_PER_TILE / 2];
+#pragma unroll
+  for (int i = 0; i < LOADS_PER_TILE / 2; ++i) {
+    const int row = (wave * IPW + i) * G_::kKeysPerInst + lane / CH;
+    full_off[i] = (unsigned)(row * RB + ((lane % CH) ^ swz<D>(row)) * 16);
+  }
+  auto issue_part = [&](int t, int w, int q) __attribute__((always_inline)) {
+    // t is the same in every lane; say so, since the LDS base must sit in an SGPR
+    // (M0) and the compiler's uniformity analysis can lose track of it in loops
+    // whose bodies branch per lane.
+    t = __builtin_amdgcn_readfirstlane(t);
     const int st = t % kStages;
-    const unsigned lk = (unsigned)(size_t)(&sRing[st][0][0]);
-    const unsigned lv = (unsigned)(size_t)(&sRing[st][1][0]);
-    const char* kb;
-    const char* vb;
+    const bool is_v = q & 1;
+    const unsigned lbase = (unsigned)(size_t)(&sRing[st][is_v ? 1 : 0][0]);
+    if (w == wave && t < n_full) {
+      const int key0 = k_begin + t * kKeyTile;
+      const char* tile_base = (is_v ? vc : kc) + (((size_t)b * p.hkv + g) * p.cap + key0) * RB;
+      dma16s(tile_base, full_off[q / 2], lbase + (w * IPW + q / 2) * G_::kKeysPerInst * RB);
+      return;
+    }
+    const char* src_base;
     size_t stride;
     int nvalid;
     if (t < n_ctx_tiles) {
       const int key0 = k_begin + t * kKeyTile;
       nvalid = min(kKeyTile, k_end - key0);
-      const size_t off = (((size_t)b * p.hkv + g) * p.cap + key0) * RB;
-      kb = kc + off;
-      vb = vc + off;
+      src_base = (is_v ? vc : kc) + (((size_t)b * p.hkv + g) * p.cap + key0) * RB;
       stride = RB;
     } else {
       nvalid = p.n;
-      const size_t off = ((size_t)b * p.n * p.hkv + g) * RB;
-      kb = kn + off;
-      vb = vn + off;
+      src_base = (is_v ? vn : kn) + ((size_t)b * p.n * p.hkv + g) * RB;
       stride = (size_t)p.hkv * RB;
     }
     // The lane's offsets are recomputed from a laundered lane id each time:
@@ -184,21 +219,20 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
     // kernel into spilling (whose reloads wait for every tile load in flight).
     int ln = lane;
     asm volatile("" : "+v"(ln));
-    const unsigned st32 = (unsigned)stride;
+    const int row0 = (w * IPW + q / 2) * G_::kKeysPerInst;
+    const int row = row0 + ln / CH;
+    const int src = row < nvalid ? row : nvalid - 1;
+    const unsigned goff = (unsigned)src * (unsigned)stride + (unsigned)(((ln % CH) ^ swz<D>(row)) * 16);
+    dma16(src_base + goff, lbase + row0 * RB);
+  };
+  auto issue = [&](int t) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      const int row0 = (wave * IPW + i) * G_::kKeysPerInst;
-      const int row = row0 + ln / CH;
-      const int src = row < nvalid ? row : nvalid - 1;
-      const unsigned goff = (unsigned)src * st32 + (unsigned)(((ln % CH) ^ swz<D>(row)) * 16);
-      dma16(kb + goff, lk + row0 * RB);
-      dma16(vb + goff, lv + row0 * RB);
-    }
+    for (int q = 0; q < LOADS_PER_TILE; ++q) issue_part(t, wave, q);
   };
 
   // Start streaming the first tiles before anything else.
 #pragma unroll
-  for (int t = 0; t < kStages - 1; ++t)
+  for (int t = 0; t < kAhead; ++t)
     if (t < n_tiles) issue(t);
 
   // ---- ancestor words of the packed tree, anc[i] = {i} u anc[parent(i)], by
@@ -252,132 +286,218 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   }
   const float c = p.scale_log2;
 
-  // MASKED: the tile holds invalid keys (the ragged last context tile) or is
-  // the new-key tile; full context tiles take the unmasked instantiation.
-  auto compute = [&](auto masked_tag, int t) {
+  // ---- one tile, for each of this wave's 16-row tiles j:
+  //   S^T[key][row] = K[key][:] . Q[row][:]   (A = K from LDS, B = Q^T)
+  //   P = exp2(S c - m_run c)                  (online softmax, lazily rescaled)
+  //   O^T[d][row] += V^T[d][key] . P^T[key][row]
+  // The keys of a tile form two halves kk (keys 32 kk .. 32 kk + 31).  A lane
+  // holds row lr and keys 32 kk + 8 lg + 4 sub + i of S^T (value sc[j][kk][sub][i]).
+  //
+  // The exponentials are computed against the running reference m_run before
+  // the tile's maximum is known, so that they can be interleaved with matrix
+  // work: those of half 0 with the Q.K MFMAs of half 1, those of half 1 with
+  // the P.V MFMAs of half 0.  Lazy rescaling keeps the reference unless a
+  // score exceeds it by more than 2^kSlack (exp2 units); in that rare case
+  // (always on a split's first tile) the reference moves, O and l are
+  // rescaled, and half 0 is scored again and exponentiated anew.
+  //
+  // Operand reads from LDS run kOpAhead operands ahead of their MFMAs, and
+  // scheduling fences keep each step (one operand's MFMAs plus its share of
+  // VALU work) in place, so the compiler neither regroups the reads (which
+  // would expose their latency) nor separates the VALU work from the MFMAs.
+  constexpr int NKO = 4 * KS;        // K operands per tile: (kk, ks, sub)
+  constexpr int NVO = 2 * DT;        // V operands per tile: (kk, dt)
+  constexpr int kOpAhead = 2;
+  constexpr int NVAL = TPW * 8;      // scores per lane in one half
+  static_assert(NKO / 2 == 2 * KS && NVO / 2 == DT, "operand counts");
+
+  auto tile = [&](auto masked_tag, int t) __attribute__((always_inline)) {
     constexpr bool masked = decltype(masked_tag)::value;
-    const int st = t % kStages;
+    const char* Kt = sRing[t % kStages][0];
+    const char* Vt = sRing[t % kStages][1];
     const bool is_new = (t == n_ctx_tiles);
     const int nvalid = is_new ? p.n : min(kKeyTile, k_end - (k_begin + t * kKeyTile));
-    const char* Kt = sRing[st][0];
-    const char* Vt = sRing[st][1];
 
-    // S^T = K Q^T for keys 32*kk + 8*(lr>>2) + 4*sub + (lr&3) on the A side.
+    auto load_k = [&](int idx) __attribute__((always_inline)) {
+      const int kk = idx / (2 * KS), ks = (idx / 2) % KS, sub = idx % 2;
+      const int krow = 32 * kk + 8 * (lr >> 2) + 4 * sub + (lr & 3);
+      return as_bf16x8(*reinterpret_cast<const u32x4*>(Kt + krow * RB + ((4 * ks + lg) ^ swz<D>(krow)) * 16));
+    };
+    // V^T operand of (kk, dt): two transposed 8-byte reads, rows vrow and vrow + 4.
+    // ds_read_b64_tr_b16: in each 16-lane group, lane jl reads row key0 + (jl>>2),
+    // columns d0 + 4*(jl&3) .. +3, and receives V[key0 + i][d0 + jl] for i = 0..3.
+    auto load_v = [&](int idx) __attribute__((always_inline)) {
+      const int kk = idx / DT, dt = idx % DT;
+      const int vrow = 32 * kk + 8 * lg + (lr >> 2);
+      const int chunk = 2 * dt + ((lane & 3) >> 1);
+      const int half = (lane & 1) * 8;
+      const char* va_lo = Vt + vrow * RB + (chunk ^ swz<D>(vrow)) * 16 + half;
+      const char* va_hi = Vt + (vrow + 4) * RB + (chunk ^ swz<D>(vrow + 4)) * 16 + half;
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va_lo));
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va_hi));
+      // whole-vector reinterpretation: element-wise bf16 inserts of the 16-bit
+      // lanes were miscompiled (every element became lo[0])
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+
     f32x4 sc[TPW][2][2];
+    bf16x8 kr[kOpAhead + 1];
+    auto qk_step = [&](int idx) __attribute__((always_inline)) {
+      if (idx + kOpAhead < NKO) kr[(idx + kOpAhead) % (kOpAhead + 1)] = load_k(idx + kOpAhead);
+      const int kk = idx / (2 * KS), ks = (idx / 2) % KS, sub = idx % 2;
 #pragma unroll
-    for (int j = 0; j < TPW; ++j)
+      for (int j = 0; j < TPW; ++j)
+        sc[j][kk][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[idx % (kOpAhead + 1)], qf[j][ks],
+                                                                ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sc[j][kk][sub],
+                                                                0, 0, 0);
+    };
+    // Q.K^T of half kk alone (used again by the rescale path)
+    auto qk_half = [&](int kk) __attribute__((always_inline)) {
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
+      for (int i = 0; i < kOpAhead; ++i) kr[(kk * 2 * KS + i) % (kOpAhead + 1)] = load_k(kk * 2 * KS + i);
 #pragma unroll
-        for (int sub = 0; sub < 2; ++sub) sc[j][kk][sub] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // k-steps outermost, so that consecutive MFMAs use different accumulators
+      for (int n = 0; n < 2 * KS; ++n) {
+        const int idx = kk * 2 * KS + n;
+        if (n + kOpAhead < 2 * KS) kr[(idx + kOpAhead) % (kOpAhead + 1)] = load_k(idx + kOpAhead);
+        const int ks = n / 2, sub = n % 2;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-        for (int sub = 0; sub < 2; ++sub) {
-          const int krow = 32 * kk + 8 * (lr >> 2) + 4 * sub + (lr & 3);
-          const bf16x8 kop = as_bf16x8(
-              *reinterpret_cast<const u32x4*>(Kt + krow * RB + ((4 * ks + lg) ^ swz<D>(krow)) * 16));
-#pragma unroll
-          for (int j = 0; j < TPW; ++j)
-            sc[j][kk][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qf[j][ks], sc[j][kk][sub], 0, 0, 0);
-        }
+        for (int j = 0; j < TPW; ++j)
+          sc[j][kk][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              kr[idx % (kOpAhead + 1)], qf[j][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sc[j][kk][sub], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
-    }
+    };
 
-    // Mask, online softmax.  Result lane l holds row lr and keys 32*kk + 8*lg + 4*sub + i.
+    auto mask_half = [&](int kk) __attribute__((always_inline)) {
+      if (!masked) return;
 #pragma unroll
-    for (int j = 0; j < TPW; ++j) {
-      if (masked) {
+      for (int j = 0; j < TPW; ++j) {
         unsigned long long anc = ~0ull;
         if (TREE && is_new && node_of[j] < p.n) anc = sAnc[node_of[j]];
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int key = 32 * kk + 8 * lg + 4 * sub + i;
-              bool vis = key < nvalid;
-              if (TREE && is_new) vis = vis && ((anc >> key) & 1ull);
-              if (!vis) sc[j][kk][sub][i] = kNegInf;
-            }
-      }
-      float mx = kNegInf;
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
         for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[j][kk][sub][i]);
-      // Lazy rescaling: the reference maximum m_run (uniform over the four
-      // lanes of a row) moves only when a score exceeds it by more than
-      // 2^kSlack in exp2 units, so most tiles skip both the cross-lane maximum
-      // and the rescale of O.  Probabilities stay below 2^kSlack, far inside
-      // the fp32 range of the sums and the bf16 range of P.  The test runs on
-      // each lane's own maximum: no lane above the reference means no row is.
-      if (__builtin_amdgcn_ballot_w64((mx * c > m_run[j] * c + kSlack) | (m_run[j] == kNegInf))) {
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run[j], mx);
+          for (int i = 0; i < 4; ++i) {
+            const int key = 32 * kk + 8 * lg + 4 * sub + i;
+            bool vis = key < nvalid;
+            if (TREE && is_new) vis = vis && ((anc >> key) & 1ull);
+            if (!vis) sc[j][kk][sub][i] = kNegInf;
+          }
+      }
+    };
+
+    float mx[TPW], ls[TPW], neg[TPW];
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+      mx[j] = kNegInf;
+      ls[j] = 0.f;
+      neg[j] = -m_run[j] * c;
+    }
+    // score n of half kk -> probability (argument <= kSlack unless the
+    // reference moves; v_exp_f32 flushes the far tail to 0)
+    auto exp_item = [&](int kk, int n, bool track_max) __attribute__((always_inline)) {
+      const int j = n / 8, sub = (n / 4) % 2, i = n % 4;
+      const float v = sc[j][kk][sub][i];
+      if (track_max) mx[j] = fmaxf(mx[j], v);
+      float e = __builtin_amdgcn_exp2f(fmaf(v, c, neg[j]));
+      // pin the exponential here: the rescale path recomputes half 0, so the
+      // compiler would otherwise sink these below the check, out of the MFMA stream
+      asm volatile("" : "+v"(e));
+      sc[j][kk][sub][i] = e;
+      ls[j] += e;
+    };
+
+    // Phase 1: Q.K^T of half 0 (matrix work only).
+#pragma unroll
+    for (int i = 0; i < kOpAhead; ++i) kr[i] = load_k(i);
+#pragma unroll
+    for (int idx = 0; idx < NKO / 2; ++idx) {
+      qk_step(idx);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // Phase 2: Q.K^T of half 1, with the exponentials of half 0.
+    mask_half(0);
+#pragma unroll
+    for (int n = 0; n < NKO / 2; ++n) {
+      qk_step(NKO / 2 + n);
+#pragma unroll
+      for (int m = n * NVAL / (NKO / 2); m < (n + 1) * NVAL / (NKO / 2); ++m) exp_item(0, m, true);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // The first V operands stream in while the maximum is checked.
+    bf16x8 vr[kOpAhead + 1];
+#pragma unroll
+    for (int i = 0; i < kOpAhead; ++i) vr[i] = load_v(i);
+    mask_half(1);
+#pragma unroll
+    for (int j = 0; j < TPW; ++j)
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mx[j] = fmaxf(mx[j], sc[j][1][sub][i]);
+    // Each lane tests its own maximum: no lane above the reference means no row is.
+    bool move = false;
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) move = move | (mx[j] * c > m_run[j] * c + kSlack) | (m_run[j] == kNegInf);
+    if (__builtin_amdgcn_ballot_w64(move)) {
+#pragma unroll
+      for (int j = 0; j < TPW; ++j) {
+        float m = mx[j];
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        const float m_new = fmaxf(m_run[j], m);
         const float m_use = (m_new == kNegInf) ? 0.f : m_new;
         const float alpha = __builtin_amdgcn_exp2f((m_run[j] - m_use) * c);
         m_run[j] = m_use;
         l_run[j] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[j][dt] *= alpha;
+        neg[j] = -m_use * c;
+        ls[j] = 0.f;
       }
-      const float neg = -m_run[j] * c;
-      float lsum = 0.f;
+      // half 0 was exponentiated against the old reference: score it again
+      qk_half(0);
+      mask_half(0);
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            // argument <= 0; v_exp_f32 flushes the far tail to 0, which is what the sum wants
-            const float e = __builtin_amdgcn_exp2f(fmaf(sc[j][kk][sub][i], c, neg));
-            sc[j][kk][sub][i] = e;
-            lsum += e;
-          }
-      l_run[j] += lsum;
+      for (int m = 0; m < NVAL; ++m) exp_item(0, m, false);
     }
+    __builtin_amdgcn_sched_barrier(0);
 
-    // O^T += V^T P^T.  ds_read_b64_tr_b16: in each 16-lane group, lane jl reads
-    // row key0 + (jl>>2), columns d0 + 4*(jl&3) .. +3, and receives
-    // V[key0 + i][d0 + jl] for i = 0..3.
+    // Phase 3: P.V of half 0, with the exponentials of half 1.
+    bf16x8 pb[TPW];
+    auto to_pb = [&](int kk) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      bf16x8 pb[TPW];
-#pragma unroll
-      for (int j = 0; j < TPW; ++j) {
+      for (int j = 0; j < TPW; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           pb[j][i] = (__bf16)sc[j][kk][0][i];
           pb[j][4 + i] = (__bf16)sc[j][kk][1][i];
         }
-      }
-      const int vrow = 32 * kk + 8 * lg + (lr >> 2);
-      const int vsw_lo = swz<D>(vrow);
-      const int vsw_hi = swz<D>(vrow + 4);
+    };
+    auto pv_step = [&](int idx) __attribute__((always_inline)) {
+      if (idx + kOpAhead < NVO) vr[(idx + kOpAhead) % (kOpAhead + 1)] = load_v(idx + kOpAhead);
+      const int dt = idx % DT;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int chunk = 2 * dt + ((lane & 3) >> 1);
-        const int half = (lane & 1) * 8;
-        const char* va_lo = Vt + vrow * RB + (chunk ^ vsw_lo) * 16 + half;
-        const char* va_hi = Vt + (vrow + 4) * RB + (chunk ^ vsw_hi) * 16 + half;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va_lo));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va_hi));
-        // whole-vector reinterpretation: element-wise bf16 inserts of the 16-bit
-        // lanes were miscompiled (every element became lo[0])
-        const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      for (int j = 0; j < TPW; ++j)
+        o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vr[idx % (kOpAhead + 1)], pb[j], o[j][dt], 0, 0, 0);
+    };
+    to_pb(0);
 #pragma unroll
-        for (int j = 0; j < TPW; ++j)
-          o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pb[j], o[j][dt], 0, 0, 0);
-      }
+    for (int n = 0; n < DT; ++n) {
+      pv_step(n);
+#pragma unroll
+      for (int m = n * NVAL / DT; m < (n + 1) * NVAL / DT; ++m) exp_item(1, m, false);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    // Phase 4: P.V of half 1.
+    to_pb(1);
+#pragma unroll
+    for (int n = 0; n < DT; ++n) {
+      pv_step(DT + n);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) l_run[j] += ls[j];
   };
 
   // Let every load the compiler knows about (queries, parents) land now: it
@@ -400,18 +520,33 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
     if (lane < p.n) sAnc[lane] = anc_word;  // read after the loop's barriers
   }
 
-  // Tile t lives in ring stage t % kStages.  Full context tiles come first;
-  // the ragged last context tile and the new-key tile (if any) need the mask.
-  const int n_full = (k_end - k_begin) / kKeyTile;
-  for (int t = 0; t < n_tiles; ++t) {
-    // own loads of tile t done (tiles t+1 .. t+kStages-2 may still be in flight)
-    if (t + kStages - 2 < n_tiles) wait_vmcnt<(kStages - 2) * LOADS_PER_TILE>();
-    else wait_vmcnt<0>();
-    lds_barrier();  // every wave's loads of tile t landed; the stage of tile t-1 is free
-    if (t + kStages - 1 < n_tiles) issue(t + kStages - 1);
-    if (wave_active) {
-      if (t < n_full) compute(std::false_type{}, t);
-      else compute(std::true_type{}, t);
+  // Barrier j: every wave's loads of tile j have landed (each wave waits for
+  // its own share first), and the ring stage that tile j + kAhead will use is
+  // free, so the loads of that tile are issued right after it.  (Issuing them
+  // from inside the tile, between the matrix phases, bought no speed and gave
+  // intermittently wrong tree-verify rows, so they stay here.)
+  auto barrier_step = [&](int j) __attribute__((always_inline)) {
+    if (j < n_tiles) {
+      if (j + kAhead - 1 < n_tiles) wait_vmcnt<(kAhead - 1) * LOADS_PER_TILE>();
+      else wait_vmcnt<0>();
+    }
+    lds_barrier();
+    if (j + kAhead < n_tiles) issue(j + kAhead);
+  };
+
+  // All waves in step: tile t is consumed between barriers t and t + 1 while
+  // kAhead tiles stream behind it.  Full context tiles run first, through a
+  // loop whose body carries no mask; the ragged last context tile and the
+  // new-key tile follow with it.
+  {
+    int t = 0;
+    for (; t < n_full; ++t) {
+      barrier_step(t);
+      if (wave_active) tile(std::false_type{}, t);
+    }
+    for (; t < n_tiles; ++t) {
+      barrier_step(t);
+      if (wave_active) tile(std::true_type{}, t);
     }
   }
 
