@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import paper_2609_00355_amd as G
-from gpu_helpers import assert_close, ensure_lib, oracle_attention, run_attention
+from gpu_helpers import TOL, assert_close, ensure_lib, oracle_attention, run_attention
 from workloads import configs as C
 
 pytestmark = pytest.mark.gpu
@@ -111,6 +111,30 @@ def test_bf16_chain_and_star(shape):
     w = _w("verify_4k", n_tree=64, depth_cap=63)
     _check("verify", w, [200], 64, seed=7, variant="tree_dominant", tree_shape=shape,
            what=f"bf16 {shape}")
+
+
+@pytest.mark.parametrize("kind", ["draft", "verify"])
+def test_bf16_value_range(kind):
+    """Values far outside fp16 range (outputs ~ 1e6): every intermediate of
+    the bf16 path (probabilities, split partials, merge) must keep the range,
+    so the error stays at the bf16 output's relative precision."""
+    w = _w("verify_4k", batch=2)
+    n = 16 if kind == "draft" else 64
+    inp = C.attention_inputs(w, kind, n, [700, 90], 8, None, False, cap=800)
+    for key in ("v_ctx", "v_new"):
+        inp[key] = (inp[key].float() * 3.0e8).to(inp[key].dtype)
+    par = None
+    if kind == "verify":
+        par, _ = C.tree_inputs(w, 8, "best_first", n=n, batch=2)
+    out, lse = run_attention(kind, inp, par, split_keys=128)
+    ref_out, ref_lse = oracle_attention(kind, inp, par)
+    assert np.all(np.isfinite(out))
+    scale = np.abs(ref_out).max()
+    err = np.abs(out - ref_out).max()
+    print(f"[bf16 value range] {kind}: max|O| {scale:.3e}, max err {err:.3e}", flush=True)
+    assert scale > 1e5
+    assert err <= TOL["bf16"]["rel"] * scale, f"error {err:.3e} > {TOL['bf16']['rel']} x {scale:.3e}"
+    assert np.abs(lse - ref_lse).max() <= TOL["bf16"]["lse"] * max(1.0, np.abs(ref_lse).max())
 
 
 @pytest.mark.parametrize("split_keys", [64, 256, 1024, 0])
