@@ -230,22 +230,20 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
     for (int q = 0; q < LOADS_PER_TILE; ++q) issue_part(t, wave, q);
   };
 
-  // Start streaming the first tiles before anything else.
-#pragma unroll
-  for (int t = 0; t < kAhead; ++t)
-    if (t < n_tiles) issue(t);
-
   // ---- ancestor words of the packed tree, anc[i] = {i} u anc[parent(i)], by
   // pointer doubling in wave 0 (one load per node instead of a chain of
   // dependent loads): after r rounds lane i holds the nodes on its root path
   // from i up to (excluding) its 2^r-th ancestor up[i].
+  // The query and parent loads below are issued from inline assembly, like
+  // the tile loads, and waited for explicitly: the compiler counts only the
+  // loads it can see, so its own wait before their first use would be
+  // vmcnt(0) and would also wait for every tile load in flight.
   unsigned long long anc_word = 0;
   int up = -1;
-  if (TREE && has_new && wave == 0 && lane < p.n) {
-    const int par = p.parents[(size_t)b * p.n + lane];
-    up = (par >= 0 && par < lane) ? par : -1;
-    anc_word = 1ull << lane;
-  }
+  int par_raw = -1;
+  const bool load_par = TREE && has_new && wave == 0 && lane < p.n;
+  if (load_par)
+    asm volatile("global_load_dword %0, %1, off" : "=v"(par_raw) : "v"(p.parents + (size_t)b * p.n + lane) : "memory");
 
   // ---- this wave's query rows, held as MFMA B operands for the whole split.
   const int n_row_tiles = (p.rows + 15) >> 4;
@@ -270,10 +268,18 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
       node_of[j] = node;
       const __bf16* qp = q + (((size_t)b * p.n + node) * p.hq + (size_t)g * p.group + hl) * D + 8 * lg;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        qf[j][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(qp + 32 * ks));
+      for (int ks = 0; ks < KS; ++ks) {
+        u32x4 raw;
+        asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(raw) : "v"(qp + 32 * ks) : "memory");
+        qf[j][ks] = as_bf16x8(raw);
+      }
     }
   }
+
+  // Then the first tiles start streaming.
+#pragma unroll
+  for (int t = 0; t < kAhead; ++t)
+    if (t < n_tiles) issue(t);
 
   f32x4 o[TPW][DT];
   float m_run[TPW], l_run[TPW];
@@ -500,10 +506,29 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
     for (int j = 0; j < TPW; ++j) l_run[j] += ls[j];
   };
 
-  // Let every load the compiler knows about (queries, parents) land now: it
-  // cannot see the tile loads above, so a wait it would place inside the loop
-  // for a first use there (vmcnt(0)) would drain the ring on every iteration.
-  wait_vmcnt<0>();
+  // Queries and parents were issued before the tile loads, so they have
+  // landed once no more than the tile loads are outstanding.  The query
+  // registers pass through the wait so that no use moves above it.
+  if (n_tiles >= kAhead) {
+#pragma unroll
+    for (int j = 0; j < TPW; ++j)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        u32x4 raw = __builtin_bit_cast(u32x4, qf[j][ks]);
+        if (j == 0 && ks == 0)
+          asm volatile("s_waitcnt vmcnt(%1)" : "+v"(raw) : "n"(kAhead * LOADS_PER_TILE) : "memory");
+        else
+          asm volatile("" : "+v"(raw));
+        qf[j][ks] = as_bf16x8(raw);
+      }
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+  if (load_par) {
+    asm volatile("" : "+v"(par_raw));
+    up = (par_raw >= 0 && par_raw < lane) ? par_raw : -1;
+    anc_word = 1ull << lane;
+  }
 
   if (TREE && has_new && wave == 0) {
 #pragma unroll
