@@ -176,9 +176,6 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
   // [8w, 8w+8); lane i of a load writes LDS row base + i/CH, chunk slot i%CH,
   // which holds global chunk slot ^ swz(row).  Rows past the valid keys re-read
   // the last valid row: their scores are masked, so P = 0 and V is finite.
-  // A wave's share is LOADS_PER_TILE instructions; issue_part(t, w, q) issues
-  // share q of wave slot w, the K rows (q even) or the V rows (q odd) of its
-  // block q / 2.
   // Lane offsets of the wave's shares within a full context tile (all 64 rows
   // valid, row stride RB), computed once; other tiles compute theirs at issue.
   unsigned full_off[LOADS_PER_TILE / 2];
@@ -187,31 +184,40 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
     const int row = (wave * IPW + i) * G_::kKeysPerInst + lane / CH;
     full_off[i] = (unsigned)(row * RB + ((lane % CH) ^ swz<D>(row)) * 16);
   }
-  auto issue_part = [&](int t, int w, int q) __attribute__((always_inline)) {
+  auto issue = [&](int t) __attribute__((always_inline)) {
     // t is the same in every lane; say so, since the LDS base must sit in an SGPR
     // (M0) and the compiler's uniformity analysis can lose track of it in loops
     // whose bodies branch per lane.
     t = __builtin_amdgcn_readfirstlane(t);
-    const int st = t % kStages;
-    const bool is_v = q & 1;
-    const unsigned lbase = (unsigned)(size_t)(&sRing[st][is_v ? 1 : 0][0]);
-    if (w == wave && t < n_full) {
-      const int key0 = k_begin + t * kKeyTile;
-      const char* tile_base = (is_v ? vc : kc) + (((size_t)b * p.hkv + g) * p.cap + key0) * RB;
-      dma16s(tile_base, full_off[q / 2], lbase + (w * IPW + q / 2) * G_::kKeysPerInst * RB);
+    const unsigned lk = (unsigned)(size_t)(&sRing[t % kStages][0][0]);
+    const unsigned lv = (unsigned)(size_t)(&sRing[t % kStages][1][0]);
+    if (t < n_full) {
+      // one tile base for all of the wave's shares: SGPR base + lane offsets
+      const size_t off = (((size_t)b * p.hkv + g) * p.cap + k_begin + (size_t)t * kKeyTile) * RB;
+#pragma unroll
+      for (int i = 0; i < LOADS_PER_TILE / 2; ++i) {
+        const unsigned lrow = (unsigned)((wave * IPW + i) * G_::kKeysPerInst * RB);
+        dma16s(kc + off, full_off[i], lk + lrow);
+        dma16s(vc + off, full_off[i], lv + lrow);
+      }
       return;
     }
-    const char* src_base;
+    const char* kb;
+    const char* vb;
     size_t stride;
     int nvalid;
     if (t < n_ctx_tiles) {
       const int key0 = k_begin + t * kKeyTile;
       nvalid = min(kKeyTile, k_end - key0);
-      src_base = (is_v ? vc : kc) + (((size_t)b * p.hkv + g) * p.cap + key0) * RB;
+      const size_t off = (((size_t)b * p.hkv + g) * p.cap + key0) * RB;
+      kb = kc + off;
+      vb = vc + off;
       stride = RB;
     } else {
       nvalid = p.n;
-      src_base = (is_v ? vn : kn) + ((size_t)b * p.n * p.hkv + g) * RB;
+      const size_t off = ((size_t)b * p.n * p.hkv + g) * RB;
+      kb = kn + off;
+      vb = vn + off;
       stride = (size_t)p.hkv * RB;
     }
     // The lane's offsets are recomputed from a laundered lane id each time:
@@ -219,15 +225,15 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
     // kernel into spilling (whose reloads wait for every tile load in flight).
     int ln = lane;
     asm volatile("" : "+v"(ln));
-    const int row0 = (w * IPW + q / 2) * G_::kKeysPerInst;
-    const int row = row0 + ln / CH;
-    const int src = row < nvalid ? row : nvalid - 1;
-    const unsigned goff = (unsigned)src * (unsigned)stride + (unsigned)(((ln % CH) ^ swz<D>(row)) * 16);
-    dma16(src_base + goff, lbase + row0 * RB);
-  };
-  auto issue = [&](int t) __attribute__((always_inline)) {
 #pragma unroll
-    for (int q = 0; q < LOADS_PER_TILE; ++q) issue_part(t, wave, q);
+    for (int i = 0; i < LOADS_PER_TILE / 2; ++i) {
+      const int row0 = (wave * IPW + i) * G_::kKeysPerInst;
+      const int row = row0 + ln / CH;
+      const int src = row < nvalid ? row : nvalid - 1;
+      const unsigned goff = (unsigned)src * (unsigned)stride + (unsigned)(((ln % CH) ^ swz<D>(row)) * 16);
+      dma16(kb + goff, lk + row0 * RB);
+      dma16(vb + goff, lv + row0 * RB);
+    }
   };
 
   // ---- ancestor words of the packed tree, anc[i] = {i} u anc[parent(i)], by
