@@ -416,7 +416,6 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
       // compiler would otherwise sink these below the check, out of the MFMA stream
       asm volatile("" : "+v"(e));
       sc[j][kk][sub][i] = e;
-      ls[j] += e;
     };
 
     // Phase 1: Q.K^T of half 0 (matrix work only).
@@ -465,7 +464,6 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[j][dt] *= alpha;
         neg[j] = -m_use * c;
-        ls[j] = 0.f;
       }
       // half 0 was exponentiated against the old reference: score it again
       qk_half(0);
@@ -477,14 +475,24 @@ __global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams 
 
     // Phase 3: P.V of half 0, with the exponentials of half 1.
     bf16x8 pb[TPW];
+    // Probabilities of half kk as the bf16 B operand of P.V; the row sum l
+    // is taken from these same bf16 values (two per v_dot2c_f32_bf16), so
+    // numerator and denominator use identical weights.
     auto to_pb = [&](int kk) __attribute__((always_inline)) {
+      typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-      for (int j = 0; j < TPW; ++j)
+      for (int j = 0; j < TPW; ++j) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           pb[j][i] = (__bf16)sc[j][kk][0][i];
           pb[j][4 + i] = (__bf16)sc[j][kk][1][i];
         }
+        ls[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 0, 1), ones, ls[j], false);
+        ls[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 2, 3), ones, ls[j], false);
+        ls[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 4, 5), ones, ls[j], false);
+        ls[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 6, 7), ones, ls[j], false);
+      }
     };
     auto pv_step = [&](int idx) __attribute__((always_inline)) {
       if (idx + kOpAhead < NVO) vr[(idx + kOpAhead) % (kOpAhead + 1)] = load_v(idx + kOpAhead);
