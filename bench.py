@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--verify-sweep", action="store_true",
+                    help="instead of the round, time the tree-verify attention alone at tree widths "
+                         "16, 32, 48 and 64 (one JSON line each) and exit")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench "
                          "with --calibrate-copy into profiles/traffic.json, then exit")
@@ -177,6 +180,44 @@ def cpu_baseline(inputs, budget_s):
                       f"numpy float64), scaled to the full round; {dt:.1f} s"}
 
 
+def verify_sweep(args, w, G, C, torch, np, dev):
+    """Verify attention cost against tree width at the workload's context: the
+    same context for every width, a best-first tree of n rows per sequence."""
+    ctx = C.context_lengths(w)
+    for n in (16, 32, 48, 64):
+        sets = []
+        for r in range(args.sets):
+            inp = C.attention_inputs(w, "verify", n, ctx, seed=r)
+            par, _ = C.tree_inputs(w, r, "best_first", n=n, batch=w.batch)
+            vv = {k: (t.to(dev) if torch.is_tensor(t) else t) for k, t in inp.items()}
+            call, out, _ = G.prepare_tree_verify_attn(vv["q"], vv["k_ctx"], vv["v_ctx"], vv["k_new"],
+                                                      vv["v_new"], vv["ctx_lens"], par.to(dev))
+            sets.append((call, vv, par, out))
+        torch.cuda.synchronize()
+        for i in range(args.warmup):
+            sets[i % len(sets)][0]()
+        reps = max(args.steps, 20)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in evs:
+            a.record()
+            b.record()
+        torch.cuda.synchronize()
+        for i in range(reps):
+            G.glance_set_kernel_events(*evs[i])
+            sets[i % len(sets)][0]()
+        torch.cuda.synchronize()
+        us = float(np.median([a.elapsed_time(b) for a, b in evs]) * 1e3)
+        par0 = sets[0][2]
+        vis = tree_visible_pairs(par0.numpy())
+        fl = attn_flops(w, ctx, n, vis)
+        kvb = kv_bytes(w, ctx)
+        print(json.dumps({"mode": "verify_sweep", "workload": w.name, "tree_rows": n, "us": round(us, 2),
+                          "tflops": round(fl / us / 1e6, 1), "mfma_frac": round(fl / us / 1e6 / MFMA_BF16_PEAK_TFLOPS, 3),
+                          "kv_gbps": round(kvb / us / 1e3, 1)}), flush=True)
+        del sets
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.traffic_from:
@@ -202,6 +243,9 @@ def main():
     dev = torch.device("cuda:0")
 
     w = C.WORKLOADS[args.workload]
+    if args.verify_sweep:
+        verify_sweep(args, w, G, C, torch, np, dev)
+        return
     t_gen = time.perf_counter()
     inputs = C.round_inputs(w, seed=0)
     t_gen = time.perf_counter() - t_gen
