@@ -241,3 +241,61 @@ def round_inputs(w, seed=0, poison=False, tree_shape="best_first", variant=None)
 def custom_workload(base, **kw):
     """A copy of a named workload with some fields replaced (for edge-case tests)."""
     return dataclasses.replace(WORKLOADS[base] if isinstance(base, str) else base, **kw)
+
+
+_T_DRAFT_LOGITS, _T_DRAFT_PLANT, _T_ROOTS = 9, 10, 11
+
+
+def draft_logits(w, seed=0, batch=None, horizon=None, vocab=None, variant=None, dtype=None):
+    """Drafter logits [batch][L][V] at offsets j = 1..L (L = block size - 1 by default).
+
+    The block head's rows are not available (no weights), so these mimic a
+    confident drafter whose certainty fades with the offset: background logits
+    ~ N(0, 1), plus at every offset four planted tokens (distinct, uniform)
+    whose logits are  top_j - 1.5 r - U(0, 0.5)  for r = 0..3, with top_j falling
+    linearly from 16 at j = 1 to 8 at j = L.  Against the ~log(V) + 0.5 = 12.4
+    log-normaliser of the background this puts q_1(best) near 0.97 and
+    q_L(best) near 0.01, so the top-63 trees reach depth 7-8 along a
+    high-probability spine with side branches, as the paper's
+    top-N-by-product trees do.
+
+    variant   None, "ties" (every offset's best planted logit copied onto two
+              more tokens: exact bf16/fp32 ties), "uniform" (all logits 0),
+              "masked" (all but 5 tokens per offset at -inf)
+    """
+    batch = batch if batch is not None else w.batch
+    L = horizon if horizon is not None else w.n_draft - 1
+    V = vocab if vocab is not None else w.vocab
+    dt = dtype if dtype is not None else w.torch_dtype
+    out = torch.empty((batch, L, V), dtype=dt)
+    for b in range(batch):
+        if variant == "uniform":
+            out[b] = 0.0
+            continue
+        rows = _randn((L, V), (w.cfg_id, _T_DRAFT_LOGITS, seed, b), 1.0)
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(
+            [w.cfg_id, _T_DRAFT_PLANT, seed, b])))
+        for j in range(L):
+            top = 16.0 - 8.0 * (j / max(L - 1, 1))
+            k = min(4, V)
+            toks = rng.choice(V, size=min(k + 2, V), replace=False)
+            for r in range(k):
+                rows[j, int(toks[r])] = top - 1.5 * r - rng.uniform(0.0, 0.5)
+            if variant == "ties":
+                for t in toks[k:]:
+                    rows[j, int(t)] = rows[j, int(toks[0])]
+            if variant == "masked":
+                keep = np.zeros(V, dtype=bool)
+                keep[toks[:k]] = True
+                keep[int(rng.integers(0, V))] = True
+                rows[j, torch.as_tensor(~keep)] = float("-inf")
+        out[b] = rows.to(dt)
+    return out
+
+
+def draft_roots(w, seed=0, batch=None, vocab=None):
+    """The pending root token b of every sequence (uniform over the vocabulary)."""
+    batch = batch if batch is not None else w.batch
+    V = vocab if vocab is not None else w.vocab
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([w.cfg_id, _T_ROOTS, seed])))
+    return torch.as_tensor(rng.integers(0, V, size=batch).astype(np.int32))
