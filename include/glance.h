@@ -16,7 +16,12 @@
  *                            (vocabulary argmax, lowest index on ties) and the
  *                            walk of Algorithm 1: the longest root-to-node path
  *                            whose every edge carries the parent row's argmax,
- *                            plus the bonus token that becomes the next root.
+ *                            plus the bonus token that becomes the next root;
+ *   glance_build_tree        the candidate tree of Algorithm 1's second step:
+ *                            the N strings of highest plug-in score
+ *                            prod_j q_j(y_j) over the drafter's marginals
+ *                            (Assumption 1, Sec. 3.2; Sec. 3.3), as parent
+ *                            and token arrays ready for tree verification.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -163,6 +168,51 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    int32_t path_stride, int32_t* next_root, void* workspace,
                                    size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Draft tree builder (Algorithm 1, second step; Sec. 3.3 with the plug-in
+ * score of Assumption 1, Sec. 3.2).  From the drafter's logits z_j at offsets
+ * j = 1..horizon, q_j = softmax(z_j), keep the `budget` strings y_{1:l}
+ * (1 <= l <= horizon) of highest score  s(y) = sum_{j<=l} log q_j(y_j)  and
+ * pack them as a tree below the root b.
+ *
+ *   draft_logits  device, dtype logits_dtype (F32 or BF16); sequence b's
+ *                 offset-j row is the `vocab` values at element offset
+ *                 b * seq_stride + (j - 1) * vocab.  NaN and +inf are outside
+ *                 the contract (results unspecified, memory-safe); -inf is a
+ *                 token of probability 0, and a row of all -inf gives
+ *                 log q = -inf throughout.
+ *   seq_stride    elements between sequences, >= horizon * vocab (e.g. the
+ *                 block head's [batch][B][vocab] rows with row 0, the root's,
+ *                 skipped: pointer + vocab and seq_stride = B * vocab)
+ *   roots         device [batch] int32, the pending root token b
+ *   parents       device [batch][budget + 1] int32 out: -1 for node 0 (the
+ *                 root), then 0 <= parents[i] < i
+ *   tokens        device [batch][budget + 1] int32 out: roots[b], then the
+ *                 token on the edge into each node
+ *   scores        device [batch][budget + 1] float32 out, or NULL: 0 for the
+ *                 root, then s(y) of each node's string
+ *   workspace     device, >= glance_tree_workspace_size(...) bytes, 256-byte aligned
+ *
+ * Nodes 1..budget are the kept strings in ranking order: score descending,
+ * then the shorter string, then the string whose tokens rank better offset by
+ * offset (a token's rank at an offset is its place in logit-descending,
+ * index-ascending order).  The kept set is prefix-closed and every node's
+ * children carry the best-ranked tokens of their offset.  Scores are fp32:
+ * log q = z - logsumexp(z), summed from the first offset on; strings whose
+ * scores differ by less than the rounding of that sum may be ranked either
+ * way.
+ *   1 <= horizon <= 15, 1 <= budget <= 63 (so budget + 1 <= 64 rows fit
+ *   glance_tree_verify_attn), 1 <= vocab <= 2^30, batch * horizon <= 65535,
+ *   and at least `budget` strings of length <= horizon must exist.
+ */
+glance_status glance_build_tree(int32_t batch, int32_t horizon, int32_t vocab, int32_t budget,
+                                glance_dtype logits_dtype, const void* draft_logits, int64_t seq_stride,
+                                const int32_t* roots, int32_t* parents, int32_t* tokens, float* scores,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes glance_build_tree needs (0 if the sizes are invalid). Host only. */
+size_t glance_tree_workspace_size(int32_t batch, int32_t horizon, int32_t vocab, int32_t budget);
+
 /* Workspace bytes an attention call with shape *s needs (0 if *s is invalid).
  * The same size serves the draft and the verify entry point. Host only. */
 size_t glance_attn_workspace_size(const glance_attn_shape* s);
@@ -187,11 +237,12 @@ const char* glance_status_string(glance_status status);
 const char* glance_last_error(void);
 
 /*
- * Profiling hook.  When both events are non-NULL, the next attention or
- * accept call on this thread records `start` on its stream right before its
- * main kernel (the split-KV attention kernel, or the vocabulary argmax
- * kernel) and `stop` right after it, then forgets the pair.  Arguments are
- * hipEvent_t handles created by the caller.  Pass NULLs to clear.
+ * Profiling hook.  When both events are non-NULL, the next attention, accept
+ * or tree-builder call on this thread records `start` on its stream right
+ * before its main kernel (the split-KV attention kernel, the vocabulary
+ * argmax kernel, or both passes of the tree builder) and `stop` right after
+ * it, then forgets the pair.  Arguments are hipEvent_t handles created by
+ * the caller.  Pass NULLs to clear.
  */
 glance_status glance_set_kernel_events(void* start_event, void* stop_event);
 

@@ -11,10 +11,12 @@ missing or a GPU is absent, the calls raise.
     glance_block_draft_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens) -> (out, lse)
     glance_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents) -> (out, lse)
     glance_greedy_accept(logits, parents, tokens) -> dict(argmax, accept_len, accept_path, next_root)
+    glance_build_tree(draft_logits, roots, budget) -> dict(parents, tokens, scores)
 
 Layouts: q, out [batch][n][Hq][D]; k_ctx, v_ctx [batch][Hkv][capacity][D];
 k_new, v_new [batch][n][Hkv][D]; ctx_lens [batch] int32; parents, tokens
-[batch][n] int32; logits [batch][n][vocab].
+[batch][n] int32; logits [batch][n][vocab]; draft_logits [batch][rows][vocab]
+(rows first_row .. first_row + horizon - 1 are the drafter's offsets 1..L).
 """
 
 import ctypes
@@ -53,6 +55,9 @@ _SIGS = {
                                                _P, _P, _SZ, _P]),
     "glance_greedy_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P, _P, _I32,
                                             _P, _P, _SZ, _P]),
+    "glance_build_tree": (ctypes.c_int, [_I32, _I32, _I32, _I32, ctypes.c_int, _P, ctypes.c_int64, _P, _P,
+                                         _P, _P, _P, _SZ, _P]),
+    "glance_tree_workspace_size": (_SZ, [_I32, _I32, _I32, _I32]),
     "glance_attn_workspace_size": (_SZ, [ctypes.POINTER(AttnShape)]),
     "glance_accept_workspace_size": (_SZ, [_I32, _I32, _I32]),
     "glance_validate_tree": (ctypes.c_int, [_I32, _P, _P, _I32]),
@@ -117,6 +122,10 @@ def glance_attn_workspace_size(shape):
 
 def glance_accept_workspace_size(batch, n_nodes, vocab):
     return int(lib().glance_accept_workspace_size(int(batch), int(n_nodes), int(vocab)))
+
+
+def glance_tree_workspace_size(batch, horizon, vocab, budget):
+    return int(lib().glance_tree_workspace_size(int(batch), int(horizon), int(vocab), int(budget)))
 
 
 def glance_set_kernel_events(start, stop):
@@ -272,6 +281,60 @@ def glance_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None
     return outputs
 
 
+def _tree_args(draft_logits, roots, budget, first_row, horizon, outputs, workspace, stream, want_scores):
+    torch = _torch()
+    _dev(draft_logits, "draft_logits", ndim=3)
+    code = _dtype_code(draft_logits)
+    batch, rows, vocab = draft_logits.shape
+    first_row = int(first_row)
+    horizon = int(horizon if horizon is not None else rows - first_row)
+    if first_row < 0 or horizon < 1 or first_row + horizon > rows:
+        raise ValueError(f"rows {first_row}..{first_row + horizon - 1} are not in draft_logits' {rows} rows")
+    _dev(roots, "roots", torch.int32, 1)
+    if roots.shape[0] != batch:
+        raise ValueError("roots must have one entry per sequence")
+    dev = draft_logits.device
+    n = int(budget) + 1
+    if outputs is None:
+        outputs = {
+            "parents": torch.empty((batch, n), dtype=torch.int32, device=dev),
+            "tokens": torch.empty((batch, n), dtype=torch.int32, device=dev),
+            "scores": torch.empty((batch, n), dtype=torch.float32, device=dev) if want_scores else None,
+        }
+    for name, dt in (("parents", torch.int32), ("tokens", torch.int32), ("scores", torch.float32)):
+        t = outputs.get(name)
+        if t is not None:
+            _dev(t, name, dt, 2)
+            if tuple(t.shape) != (batch, n):
+                raise ValueError(f"{name} must be [batch][budget + 1]")
+    need = glance_tree_workspace_size(batch, horizon, vocab, budget)
+    if need == 0:
+        raise GlanceError(GLANCE_ERR_INVALID_ARG, glance_last_error())
+    ws = _workspace(need, dev, workspace)
+    base = ctypes.c_void_p(draft_logits.data_ptr() + first_row * vocab * draft_logits.element_size())
+    args = [ctypes.c_int32(batch), ctypes.c_int32(horizon), ctypes.c_int32(vocab), ctypes.c_int32(int(budget)),
+            ctypes.c_int(code), base, ctypes.c_int64(rows * vocab), _ptr(roots), _ptr(outputs["parents"]),
+            _ptr(outputs["tokens"]), _ptr(outputs.get("scores")), _ptr(ws),
+            ctypes.c_size_t(ws.numel() * ws.element_size()), _stream(stream)]
+    return args, outputs, ws
+
+
+def glance_build_tree(draft_logits, roots, budget, first_row=0, horizon=None, outputs=None, workspace=None,
+                      stream=None, want_scores=True):
+    """The budget-N draft tree of Algorithm 1's second step.
+
+    draft_logits [batch][rows][vocab]: rows first_row .. first_row + horizon - 1
+    are the drafter's offsets 1..L (first_row=1 skips the root row of a block
+    head's output).  roots [batch] int32.  Returns a dict of GPU tensors
+    parents, tokens [batch][budget + 1] int32 and scores [batch][budget + 1]
+    float32 (None if want_scores is False).
+    """
+    args, outputs, _ = _tree_args(draft_logits, roots, budget, first_row, horizon, outputs, workspace, stream,
+                                  want_scores)
+    _check(lib().glance_build_tree(*args))
+    return outputs
+
+
 # ---------------------------------------------------------------- prepared calls
 class PreparedCall:
     """A library call with all arguments checked and marshalled once.
@@ -342,3 +405,13 @@ def prepare_greedy_accept(logits, parents, tokens, path_stride=None, outputs=Non
             ctypes.c_size_t(ws.numel() * ws.element_size()), _stream(stream)]
     keep = (logits, parents, tokens, outputs, ws)
     return PreparedCall(lib().glance_greedy_accept, args, keep), outputs
+
+
+def prepare_build_tree(draft_logits, roots, budget, first_row=0, horizon=None, outputs=None, workspace=None,
+                       stream=None, want_scores=True):
+    """Returns (call, outputs): call() re-runs the tree builder into the outputs dict."""
+    args, outputs, ws = _tree_args(draft_logits, roots, budget, first_row, horizon, outputs, workspace, stream,
+                                   want_scores)
+    _check(lib().glance_build_tree(*args))
+    keep = (draft_logits, roots, outputs, ws)
+    return PreparedCall(lib().glance_build_tree, args, keep), outputs

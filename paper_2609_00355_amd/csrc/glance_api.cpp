@@ -228,6 +228,63 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
   return ok();
 }
 
+struct TreePlan {
+  glance::TreeParams p;  // sizes and workspace offsets; pointers filled per call
+  size_t off_stats, off_sketch, off_cand, off_lq, off_tok, off_count, off_ticket, off_seq, bytes;
+};
+
+glance_status tree_plan(int32_t batch, int32_t horizon, int32_t vocab, int32_t budget, TreePlan* out) {
+  if (batch < 1) return fail(GLANCE_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (horizon < 1) return fail(GLANCE_ERR_INVALID_ARG, "horizon must be >= 1 (got %d)", horizon);
+  if (horizon > glance::kTreeMaxHorizon)
+    return fail(GLANCE_ERR_UNSUPPORTED, "horizon must be <= %d (got %d)", glance::kTreeMaxHorizon, horizon);
+  if (budget < 1) return fail(GLANCE_ERR_INVALID_ARG, "budget must be >= 1 (got %d)", budget);
+  if (budget > glance::kTreeMaxBudget)
+    return fail(GLANCE_ERR_UNSUPPORTED, "budget must be <= %d (got %d)", glance::kTreeMaxBudget, budget);
+  if (vocab < 1 || vocab > (1 << 30)) return fail(GLANCE_ERR_INVALID_ARG, "vocab must be in 1..2^30");
+  // the strings of length 1..horizon must number at least `budget`
+  long long strings = 0, pw = 1;
+  for (int l = 1; l <= horizon && strings < budget; ++l) {
+    pw = pw * vocab > budget ? (long long)budget + 1 : pw * vocab;
+    strings += pw;
+  }
+  if (strings < budget)
+    return fail(GLANCE_ERR_INVALID_ARG, "budget %d exceeds the %lld strings of length <= %d over %d tokens",
+                budget, strings, horizon, vocab);
+  const long long rows = (long long)batch * horizon;
+  if (rows > 65535) return fail(GLANCE_ERR_UNSUPPORTED, "batch * horizon must be <= 65535");
+  if (rows * (long long)vocab > (1LL << 40)) return fail(GLANCE_ERR_UNSUPPORTED, "draft logits too large");
+  glance::TreeParams p = {};
+  p.batch = batch;
+  p.horizon = horizon;
+  p.vocab = vocab;
+  p.budget = budget;
+  p.k = budget < vocab ? budget : vocab;
+  p.slices = (vocab + glance::kTreeSlice - 1) / glance::kTreeSlice;
+  p.groups = 1;
+  while ((long long)p.slices * p.groups < p.k && p.groups < 64) p.groups *= 2;
+  p.wgs_per_row = (p.slices + 3) / 4;
+  TreePlan pl;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += round_up(bytes, 256);
+    return at;
+  };
+  pl.off_stats = take((size_t)rows * p.slices * sizeof(float2));
+  pl.off_sketch = take((size_t)rows * p.slices * p.groups * sizeof(float));
+  pl.off_cand = take((size_t)rows * glance::kTreeCap * sizeof(unsigned long long));
+  pl.off_lq = take((size_t)rows * 64 * sizeof(float));
+  pl.off_tok = take((size_t)rows * 64 * sizeof(int32_t));
+  pl.off_count = take((size_t)rows * sizeof(int32_t));
+  pl.off_ticket = take((size_t)rows * sizeof(int32_t));
+  pl.off_seq = take((size_t)batch * sizeof(int32_t));
+  pl.bytes = off;
+  pl.p = p;
+  *out = pl;
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -300,6 +357,68 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                    "accept kernel launch");
 }
 
+glance_status glance_build_tree(int32_t batch, int32_t horizon, int32_t vocab, int32_t budget,
+                                glance_dtype logits_dtype, const void* draft_logits, int64_t seq_stride,
+                                const int32_t* roots, int32_t* parents, int32_t* tokens, float* scores,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  TreePlan pl;
+  glance_status st = tree_plan(batch, horizon, vocab, budget, &pl);
+  if (st != GLANCE_OK) return st;
+  if (logits_dtype != GLANCE_F32 && logits_dtype != GLANCE_BF16)
+    return fail(GLANCE_ERR_UNSUPPORTED, "draft logits dtype must be GLANCE_F32 or GLANCE_BF16");
+  if (seq_stride < (int64_t)horizon * vocab)
+    return fail(GLANCE_ERR_INVALID_ARG, "seq_stride (%lld) must be >= horizon * vocab (%lld)",
+                (long long)seq_stride, (long long)horizon * vocab);
+  const size_t esz = logits_dtype == GLANCE_BF16 ? 2 : 4;
+  if (!draft_logits) return fail(GLANCE_ERR_INVALID_ARG, "draft_logits is NULL");
+  if (reinterpret_cast<uintptr_t>(draft_logits) & (esz - 1))
+    return fail(GLANCE_ERR_INVALID_ARG, "draft_logits is not %zu-byte aligned", esz);
+  struct {
+    const void* ptr;
+    const char* name;
+  } req[] = {{roots, "roots"}, {parents, "parents"}, {tokens, "tokens"}};
+  for (auto& r : req) {
+    if (!r.ptr) return fail(GLANCE_ERR_INVALID_ARG, "%s is NULL", r.name);
+    if (reinterpret_cast<uintptr_t>(r.ptr) & 3u) return fail(GLANCE_ERR_INVALID_ARG, "%s is not 4-byte aligned", r.name);
+  }
+  if (scores && (reinterpret_cast<uintptr_t>(scores) & 3u))
+    return fail(GLANCE_ERR_INVALID_ARG, "scores is not 4-byte aligned");
+  if (!workspace) return fail(GLANCE_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(GLANCE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < pl.bytes)
+    return fail(GLANCE_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes,
+                pl.bytes);
+  glance::TreeParams p = pl.p;
+  char* ws = static_cast<char*>(workspace);
+  p.logits = draft_logits;
+  p.seq_stride = seq_stride;
+  p.roots = roots;
+  p.parents = parents;
+  p.tokens = tokens;
+  p.scores = scores;
+  p.stats = reinterpret_cast<float2*>(ws + pl.off_stats);
+  p.sketch = reinterpret_cast<float*>(ws + pl.off_sketch);
+  p.cand = reinterpret_cast<unsigned long long*>(ws + pl.off_cand);
+  p.lq = reinterpret_cast<float*>(ws + pl.off_lq);
+  p.tok = reinterpret_cast<int32_t*>(ws + pl.off_tok);
+  p.count = reinterpret_cast<int32_t*>(ws + pl.off_count);
+  p.ticket = reinterpret_cast<int32_t*>(ws + pl.off_ticket);
+  p.seq_ticket = reinterpret_cast<int32_t*>(ws + pl.off_seq);
+  p.vec = (reinterpret_cast<uintptr_t>(draft_logits) & 15u) == 0 && ((size_t)vocab * esz) % 16 == 0 &&
+          ((size_t)seq_stride * esz) % 16 == 0;
+  hipEvent_t e0, e1;
+  take_events(&e0, &e1);
+  return check_hip(glance::launch_tree(p, logits_dtype == GLANCE_BF16, stream, e0, e1),
+                   "tree builder kernel launch");
+}
+
+size_t glance_tree_workspace_size(int32_t batch, int32_t horizon, int32_t vocab, int32_t budget) {
+  TreePlan pl;
+  if (tree_plan(batch, horizon, vocab, budget, &pl) != GLANCE_OK) return 0;
+  return pl.bytes;
+}
+
 size_t glance_attn_workspace_size(const glance_attn_shape* s) {
   Plan pl;
   if (make_plan(s, &pl) != GLANCE_OK) return 0;
@@ -356,6 +475,6 @@ glance_status glance_set_kernel_events(void* start_event, void* stop_event) {
   return ok();
 }
 
-int32_t glance_version(void) { return 100; }
+int32_t glance_version(void) { return 200; }
 
 }  // extern "C"

@@ -62,9 +62,48 @@ struct AcceptParams {
   int chunks, chunk_len;     // chunk_len is a multiple of 8
 };
 
+// Draft tree builder.  Limits: budget N <= kTreeMaxBudget strings below the
+// root, horizon L <= kTreeMaxHorizon offsets (five 6-bit ranks per word, three
+// words), K = min(N, vocab) ranked tokens kept per offset.
+constexpr int kTreeMaxBudget = 63;
+constexpr int kTreeMaxHorizon = 15;
+constexpr int kTreeSlice = 1024;   // values per wave in the two streaming passes
+constexpr int kTreeCap = 2048;     // candidate slots per row before the exact fallback
+
+// Layouts (row = sequence * L + offset - 1):
+//   logits  sequence b, offset j (1..L) at logits + b*seq_stride + (j-1)*vocab
+//   stats   [rows][slices] (max, sum exp(x - max)) of each 1024-value slice
+//   sketch  [rows][slices * groups] maxima of disjoint lane groups
+//   cand    [rows][kTreeCap] packed (order key, ~index) of values >= threshold
+//   lq, tok [rows][64] the row's K best tokens in rank order and their log q
+//   count, ticket [rows]; seq_ticket [batch]
+struct TreeParams {
+  const void* logits;
+  long long seq_stride;
+  const int32_t* roots;
+  int32_t* parents;
+  int32_t* tokens;
+  float* scores;
+  float2* stats;
+  float* sketch;
+  unsigned long long* cand;
+  float* lq;
+  int32_t* tok;
+  int32_t* count;
+  int32_t* ticket;
+  int32_t* seq_ticket;
+  int batch, horizon, vocab, budget;
+  int k;            // ranked tokens per offset, min(budget, vocab)
+  int slices;       // ceil(vocab / kTreeSlice)
+  int groups;       // sketch entries per slice, a power of two in 1..64
+  int wgs_per_row;  // ceil(slices / 4)
+  int vec;          // rows are 16-byte aligned: vector loads
+};
+
 hipError_t launch_attn_bf16(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_attn_f32(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_attn_merge(const AttnParams& p, bool out_bf16, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+hipError_t launch_tree(const TreeParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
 }  // namespace glance

@@ -128,6 +128,50 @@ def test_accept_argument_checks(lib):
     assert st == G.GLANCE_ERR_WORKSPACE
 
 
+def _build_tree(lib, batch=1, horizon=15, vocab=152064, budget=63, dtype=G.GLANCE_BF16, logits=FAKE,
+                stride=None, roots=FAKE, parents=FAKE, tokens=FAKE, scores=FAKE, ws=FAKE, ws_bytes=1 << 30):
+    stride = horizon * vocab if stride is None else stride
+    return lib.glance_build_tree(batch, horizon, vocab, budget, dtype, logits, stride, roots, parents, tokens,
+                                 scores, ws, ws_bytes, None)
+
+
+def test_tree_builder_workspace_size(lib):
+    a = G.glance_tree_workspace_size(4, 15, 152064, 63)
+    assert a > 0
+    # candidate lists dominate: rows x 2048 slots x 8 bytes
+    assert a >= 4 * 15 * 2048 * 8
+    assert G.glance_tree_workspace_size(8, 15, 152064, 63) > a
+    assert G.glance_tree_workspace_size(1, 15, 152064, 64) == 0
+    assert G.glance_tree_workspace_size(1, 16, 152064, 63) == 0
+    assert G.glance_tree_workspace_size(1, 2, 2, 7) == 0          # 2 + 4 strings < 7
+    assert G.glance_tree_workspace_size(1, 2, 2, 6) > 0
+
+
+@pytest.mark.parametrize("kw,code,word", [
+    (dict(batch=0), G.GLANCE_ERR_INVALID_ARG, "batch"),
+    (dict(horizon=0), G.GLANCE_ERR_INVALID_ARG, "horizon"),
+    (dict(horizon=16), G.GLANCE_ERR_UNSUPPORTED, "horizon"),
+    (dict(budget=0), G.GLANCE_ERR_INVALID_ARG, "budget"),
+    (dict(budget=64), G.GLANCE_ERR_UNSUPPORTED, "budget"),
+    (dict(vocab=3, horizon=3, budget=63), G.GLANCE_ERR_INVALID_ARG, "strings"),    # 3 + 9 + 27 < 63
+    (dict(vocab=0), G.GLANCE_ERR_INVALID_ARG, "vocab"),
+    (dict(dtype=5), G.GLANCE_ERR_UNSUPPORTED, "dtype"),
+    (dict(stride=15 * 152064 - 1), G.GLANCE_ERR_INVALID_ARG, "seq_stride"),
+    (dict(logits=None), G.GLANCE_ERR_INVALID_ARG, "draft_logits"),
+    (dict(logits=ctypes.c_void_p(0x10001)), G.GLANCE_ERR_INVALID_ARG, "aligned"),
+    (dict(roots=None), G.GLANCE_ERR_INVALID_ARG, "roots"),
+    (dict(parents=None), G.GLANCE_ERR_INVALID_ARG, "parents"),
+    (dict(tokens=ctypes.c_void_p(0x10002)), G.GLANCE_ERR_INVALID_ARG, "tokens"),
+    (dict(scores=ctypes.c_void_p(0x10002)), G.GLANCE_ERR_INVALID_ARG, "scores"),
+    (dict(ws=None), G.GLANCE_ERR_WORKSPACE, "workspace"),
+    (dict(ws=ctypes.c_void_p(0x10010)), G.GLANCE_ERR_WORKSPACE, "aligned"),
+    (dict(ws_bytes=1024), G.GLANCE_ERR_WORKSPACE, "too small"),
+])
+def test_tree_builder_argument_checks(lib, kw, code, word):
+    assert _build_tree(lib, **kw) == code
+    assert word in G.glance_last_error()
+
+
 @pytest.mark.parametrize("parents,tokens,max_depth,ok", [
     ([-1], None, 15, True),
     ([-1, 0, 0, 1, 3], [9, 1, 2, 3, 4], 15, True),
