@@ -45,6 +45,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--no-tree", action="store_true", help="skip the tree-builder measurement")
     ap.add_argument("--verify-sweep", action="store_true",
                     help="instead of the round, time the tree-verify attention alone at tree widths "
                          "16, 32, 48 and 64 (one JSON line each) and exit")
@@ -218,6 +219,46 @@ def verify_sweep(args, w, G, C, torch, np, dev):
         torch.cuda.empty_cache()
 
 
+def measure_tree_builder(args, w, G, C, torch, np, dev, stream):
+    """The tree builder (Algorithm 1, second step) on the drafter's logits of the
+    same workload: 15 offsets x vocab per sequence, budget 63.  Timed on its own
+    (it is not one of the round's attention / acceptance kernels): HIP events
+    around its four kernels, median over the steps, rotating input copies."""
+    budget = w.n_tree - 1
+    calls = []
+    for r in range(args.sets):
+        zd = C.draft_logits(w, 0).to(dev)
+        roots = C.draft_roots(w, 0).to(dev)
+        call, out = G.prepare_build_tree(zd, roots, budget, want_scores=False)
+        calls.append((call, out, zd, roots))
+    for i in range(args.warmup):
+        calls[i % len(calls)][0]()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, b in evs:
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        G.glance_set_kernel_events(*evs[i])
+        calls[i % len(calls)][0]()
+    torch.cuda.synchronize()
+    us = float(np.median([a.elapsed_time(b) for a, b in evs]) * 1e3)
+    nbytes = w.batch * (w.n_draft - 1) * w.vocab * 2
+    gbps = nbytes / us / 1e3
+    depth = []
+    par = calls[0][1]["parents"].cpu().numpy()
+    for b in range(par.shape[0]):
+        d = [0] * par.shape[1]
+        for i in range(1, par.shape[1]):
+            d[i] = d[par[b, i]] + 1
+        depth.append(max(d))
+    return {"us": round(us, 2), "kernels": "tree_stats + tree_cands + tree_rank + tree_enum",
+            "input": f"drafter logits {w.batch} x {w.n_draft - 1} x {w.vocab} bf16, budget {budget}",
+            "gbps": round(gbps, 1), "bound": "hbm", "frac": round(gbps / HBM_PEAK_GBS, 4),
+            "tree_depth": depth}
+
+
 def main():
     args = parse()
     if args.traffic_from:
@@ -377,6 +418,8 @@ def main():
     roof["traffic"] = load_traffic(dom, src)
     roof["kernel"] = per_kernel[dom]["kernel"]
 
+    tree = None if args.no_tree else measure_tree_builder(args, w, G, C, torch, np, dev, stream)
+
     acc = sets[0]["a_out"]["accept_len"].cpu().numpy()
     res = {
         "metric": "draft+verify round latency (us) and achieved KV HBM GB/s at 16k ctx, 1 MI355X",
@@ -405,6 +448,8 @@ def main():
         "synthetic_tau": round(1.0 + float(acc.mean()), 3),
         "input_gen_s": round(t_gen, 1),
     }
+    if tree is not None:
+        res["tree_builder"] = tree
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(inputs, args.cpu_seconds)
     print(json.dumps(res), flush=True)

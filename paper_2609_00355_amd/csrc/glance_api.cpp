@@ -230,7 +230,7 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
 
 struct TreePlan {
   glance::TreeParams p;  // sizes and workspace offsets; pointers filled per call
-  size_t off_stats, off_sketch, off_cand, off_lq, off_tok, off_count, off_ticket, off_seq, bytes;
+  size_t off_stats, off_sketch, off_cand, off_ccount, off_lq, off_tok, bytes;
 };
 
 glance_status tree_plan(int32_t batch, int32_t horizon, int32_t vocab, int32_t budget, TreePlan* out) {
@@ -263,7 +263,20 @@ glance_status tree_plan(int32_t batch, int32_t horizon, int32_t vocab, int32_t b
   p.slices = (vocab + glance::kTreeSlice - 1) / glance::kTreeSlice;
   p.groups = 1;
   while ((long long)p.slices * p.groups < p.k && p.groups < 64) p.groups *= 2;
-  p.wgs_per_row = (p.slices + 3) / 4;
+  // threshold buckets: four entries each when every bucket holds at least
+  // four sketch entries, else one (the sketch has >= k entries)
+  {
+    const long long S = (long long)p.slices * p.groups;
+    const int j = 4, nb = (p.k + j - 1) / j;
+    if (S / nb >= j) {
+      p.tau_buckets = nb;
+      p.tau_rank = j;
+    } else {
+      p.tau_buckets = p.k;
+      p.tau_rank = 1;
+    }
+  }
+  p.wgs_per_row = (p.slices + 4 * glance::kTreeSlicesPerWave - 1) / (4 * glance::kTreeSlicesPerWave);
   TreePlan pl;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -273,12 +286,10 @@ glance_status tree_plan(int32_t batch, int32_t horizon, int32_t vocab, int32_t b
   };
   pl.off_stats = take((size_t)rows * p.slices * sizeof(float2));
   pl.off_sketch = take((size_t)rows * p.slices * p.groups * sizeof(float));
-  pl.off_cand = take((size_t)rows * glance::kTreeCap * sizeof(unsigned long long));
+  pl.off_cand = take((size_t)rows * p.slices * glance::kTreeSliceCap * sizeof(unsigned long long));
+  pl.off_ccount = take((size_t)rows * p.slices * sizeof(int32_t));
   pl.off_lq = take((size_t)rows * 64 * sizeof(float));
   pl.off_tok = take((size_t)rows * 64 * sizeof(int32_t));
-  pl.off_count = take((size_t)rows * sizeof(int32_t));
-  pl.off_ticket = take((size_t)rows * sizeof(int32_t));
-  pl.off_seq = take((size_t)batch * sizeof(int32_t));
   pl.bytes = off;
   pl.p = p;
   *out = pl;
@@ -402,9 +413,7 @@ glance_status glance_build_tree(int32_t batch, int32_t horizon, int32_t vocab, i
   p.cand = reinterpret_cast<unsigned long long*>(ws + pl.off_cand);
   p.lq = reinterpret_cast<float*>(ws + pl.off_lq);
   p.tok = reinterpret_cast<int32_t*>(ws + pl.off_tok);
-  p.count = reinterpret_cast<int32_t*>(ws + pl.off_count);
-  p.ticket = reinterpret_cast<int32_t*>(ws + pl.off_ticket);
-  p.seq_ticket = reinterpret_cast<int32_t*>(ws + pl.off_seq);
+  p.ccount = reinterpret_cast<int32_t*>(ws + pl.off_ccount);
   p.vec = (reinterpret_cast<uintptr_t>(draft_logits) & 15u) == 0 && ((size_t)vocab * esz) % 16 == 0 &&
           ((size_t)seq_stride * esz) % 16 == 0;
   hipEvent_t e0, e1;

@@ -67,16 +67,18 @@ struct AcceptParams {
 // words), K = min(N, vocab) ranked tokens kept per offset.
 constexpr int kTreeMaxBudget = 63;
 constexpr int kTreeMaxHorizon = 15;
-constexpr int kTreeSlice = 1024;   // values per wave in the two streaming passes
-constexpr int kTreeCap = 2048;     // candidate slots per row before the exact fallback
+constexpr int kTreeSlice = 1024;   // values per slice (one wave-wide load of 16 per lane)
+constexpr int kTreeSlicesPerWave = 4;
+constexpr int kTreeSliceCap = 32;  // candidate slots per slice before the exact fallback
+constexpr int kTreeCap = 2048;     // candidates per row ranked by counting
 
 // Layouts (row = sequence * L + offset - 1):
 //   logits  sequence b, offset j (1..L) at logits + b*seq_stride + (j-1)*vocab
 //   stats   [rows][slices] (max, sum exp(x - max)) of each 1024-value slice
 //   sketch  [rows][slices * groups] maxima of disjoint lane groups
-//   cand    [rows][kTreeCap] packed (order key, ~index) of values >= threshold
+//   cand    [rows][slices][kTreeSliceCap] packed (order key, ~index) of the
+//           slice's values >= threshold; ccount [rows][slices] their number
 //   lq, tok [rows][64] the row's K best tokens in rank order and their log q
-//   count, ticket [rows]; seq_ticket [batch]
 struct TreeParams {
   const void* logits;
   long long seq_stride;
@@ -89,14 +91,14 @@ struct TreeParams {
   unsigned long long* cand;
   float* lq;
   int32_t* tok;
-  int32_t* count;
-  int32_t* ticket;
-  int32_t* seq_ticket;
+  int32_t* ccount;
   int batch, horizon, vocab, budget;
   int k;            // ranked tokens per offset, min(budget, vocab)
   int slices;       // ceil(vocab / kTreeSlice)
   int groups;       // sketch entries per slice, a power of two in 1..64
-  int wgs_per_row;  // ceil(slices / 4)
+  int tau_buckets;  // B: threshold buckets over the sketch
+  int tau_rank;     // j in 1..4: the bucket entry of rank j bounds the threshold; B * j >= k
+  int wgs_per_row;  // ceil(slices / (4 * kTreeSlicesPerWave))
   int vec;          // rows are 16-byte aligned: vector loads
 };
 
