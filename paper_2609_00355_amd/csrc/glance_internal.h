@@ -68,7 +68,7 @@ struct AcceptParams {
 constexpr int kTreeMaxBudget = 63;
 constexpr int kTreeMaxHorizon = 15;
 constexpr int kTreeSlice = 1024;   // values per slice (one wave-wide load of 16 per lane)
-constexpr int kTreeSlicesPerWave = 4;
+constexpr int kTreeSlicesPerWave = 2;
 constexpr int kTreeSliceCap = 32;  // candidate slots per slice before the exact fallback
 constexpr int kTreeCap = 2048;     // candidates per row ranked by counting
 
