@@ -14,6 +14,9 @@ the GPU path:
 * ``accept``     -- per-row vocabulary argmax and the greedy walk of Algorithm 1
   (App. B), plus an independent evaluation of the accepted length
   A(T) = max{k : Y_{1:j} in T for all j <= k} of Def. 1;
+* ``commit``     -- the commit of a round's accepted path: the keys and values of
+  the root and the accepted nodes join the context cache (Def. 1's walk
+  commits them; Eq. 1);
 * ``tree``       -- the tree builder of Sec. 3.3 (Algorithm 1, second step): the
   N strings of highest plug-in score prod_j q_j(y_j) (Assumption 1) packed as
   a prefix-closed tree, by exhaustive and by best-first enumeration;
@@ -21,4 +24,4 @@ the GPU path:
   lossless greedy equivalence of Thm. 1 (Sec. 3.3, App. A.1).
 """
 
-from . import attention, accept, tiny_model, tree  # noqa: F401
+from . import attention, accept, commit, tiny_model, tree  # noqa: F401

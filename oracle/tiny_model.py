@@ -15,7 +15,10 @@ and offers two decoders over it:
 * ``glance_decode``  -- GLANCE rounds (Algorithm 1, App. B): the pending root b and
   a candidate tree are packed into one verify pass whose attention is the
   oracle's explicit-mask attention with the ancestor mask, the node at depth d
-  sitting at position ctx + d; the rows are walked by ``oracle.accept``.
+  sitting at position ctx + d; the rows are walked by ``oracle.accept``;
+* ``glance_decode_cached`` -- the same rounds over a persistent key/value cache:
+  the verify pass reads the cache and returns every node's keys and values,
+  and the accepted path is committed into the cache by ``oracle.commit``.
 
 The tree proposer is a plug-in argument, standing in for the block head and the
 tree builder, which need trained weights.  Whatever it proposes, the committed
@@ -26,6 +29,7 @@ import numpy as np
 
 from . import attention as _attn
 from . import accept as _acc
+from . import commit as _commit
 
 
 class TinyDecoder:
@@ -146,6 +150,30 @@ class TinyDecoder:
         return self._logits(h)
 
 
+    def verify_tree_cached(self, caches, ctx, parents, tokens):
+        """The verify pass over a cache: caches[l] = (K, V) [Hkv][capacity][D] holding
+        the first ``ctx`` prefix positions.  Returns the rows' logits [n][vocab] and,
+        per layer, the nodes' keys and values [n][Hkv][D] (post-rotary, node i at
+        position ctx + depth(i))."""
+        tokens = np.asarray(tokens, dtype=np.int64)
+        parents = [int(p) for p in parents]
+        n = len(parents)
+        depth = [0] * n
+        for i in range(1, n):
+            depth[i] = depth[parents[i]] + 1
+        pos = ctx + np.asarray(depth)
+        vis = _attn.tree_visibility(parents)
+        h = self.emb[tokens]
+        new_kv = []
+        for li, lw in enumerate(self.layers):
+            q, k, v = self._qkv(lw, h, pos)
+            new_kv.append((k, v))
+            kc, vc = caches[li][0][:, :ctx], caches[li][1][:, :ctx]
+            o, _ = _attn.masked_attention_one(q, kc, vc, k, v, ctx, vis, 1.0 / np.sqrt(self.hd))
+            h = self._mlp_residual(lw, h, o)
+        return self._logits(h), new_kv
+
+
 def greedy_ar(model, prompt, n_tokens):
     """Greedy autoregressive decoding (Sec. 3.1): one full forward per token.
 
@@ -187,3 +215,41 @@ def glance_decode(model, prompt, n_tokens, propose_tree):
         out.extend(int(tokens[c]) for c in path[1:])
         out.append(int(nr))
     return out[:n_tokens], accepted
+
+
+def glance_decode_cached(model, prompt, n_tokens, propose_tree, capacity=256):
+    """GLANCE rounds over a persistent cache, committing each round's path.
+
+    Returns (generated tokens, accepted lengths, caches, ctx): caches[l] = (K, V)
+    [Hkv][capacity][D] after the last round and ctx the committed prefix length
+    (prompt + every committed token except the pending root).
+    """
+    prompt = [int(t) for t in prompt]
+    logits, pre = model.forward_causal(prompt)
+    caches = []
+    for k, v in pre:
+        kc = np.zeros((model.hkv, capacity, model.hd))
+        vc = np.zeros((model.hkv, capacity, model.hd))
+        kc[:, :len(prompt)] = np.transpose(k, (1, 0, 2))
+        vc[:, :len(prompt)] = np.transpose(v, (1, 0, 2))
+        caches.append((kc, vc))
+    ctx = len(prompt)
+    out = [int(np.argmax(logits[-1]))]
+    accepted = []
+    while len(out) < n_tokens:
+        root = out[-1]
+        parents, tokens = propose_tree(prompt + out[:-1], root)
+        rows, new_kv = model.verify_tree_cached(caches, ctx, parents, tokens)
+        am = _acc.argmax_rows(rows)
+        a, path, nr = _acc.greedy_walk(am, parents, tokens)
+        accepted.append(a)
+        path_arr = np.asarray([path], dtype=np.int64)
+        for li in range(len(caches)):
+            k_new, v_new = new_kv[li]
+            kc, vc, lens = _commit.commit_kv(caches[li][0][None], caches[li][1][None], [ctx],
+                                             k_new[None], v_new[None], [a], path_arr)
+            caches[li] = (kc[0], vc[0])
+        ctx = int(lens[0])
+        out.extend(int(tokens[c]) for c in path[1:])
+        out.append(int(nr))
+    return out[:n_tokens], accepted, caches, ctx
