@@ -17,6 +17,9 @@
  *                            walk of Algorithm 1: the longest root-to-node path
  *                            whose every edge carries the parent row's argmax,
  *                            plus the bonus token that becomes the next root;
+ *   glance_commit_path       the commit of a round: the keys and values of the
+ *                            root and the accepted nodes join the context
+ *                            cache, whose length advances (Def. 1, Eq. 1);
  *   glance_build_tree        the candidate tree of Algorithm 1's second step:
  *                            the N strings of highest plug-in score
  *                            prod_j q_j(y_j) over the drafter's marginals
@@ -169,6 +172,39 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Commit of a round's accepted path into a context cache (the walk of Def. 1
+ * commits the pending root and the accepted tokens y_1..y_a; Eq. 1 counts
+ * them with the bonus token, which becomes the next root and is not cached).
+ * The verify pass computed every node's keys and values at position
+ * ctx + depth, which for the nodes of the accepted path is exactly the slot
+ * the token takes in the prefix, so for each sequence b, with a = accept_len[b]
+ * and ctx = ctx_lens[b]:
+ *     k_ctx[b, :, ctx + i, :] = k_new[b, accept_path[b][i], :, :]    (i = 0..a)
+ *     (likewise v), then ctx_lens[b] = ctx + a + 1.
+ * The cache then equals what autoregressive decoding would have built.
+ *
+ *   k_new, v_new   device [batch][n_nodes][Hkv][D], dtype: the verify pass's
+ *                  post-rotary keys and values of the packed rows
+ *   accept_len     device [batch] int32, accept_path device [batch][path_stride]
+ *                  int32: glance_greedy_accept's outputs (node 0 first)
+ *   k_ctx, v_ctx   device [batch][Hkv][ctx_capacity][D], dtype; written in place
+ *   ctx_lens       device [batch] int32; read, then advanced in place
+ * Device data is made safe: a row count of min(a + 1, path_stride, n_nodes)
+ * (none if a < 0), the copy stops at the first path entry outside
+ * [0, n_nodes), ctx is clamped to [0, ctx_capacity], slots at or past the
+ * capacity are not written and the length stops at ctx_capacity.  The length
+ * grows by the path rows copied, so path_stride must hold a + 1 entries
+ * (>= 16 for trees of depth <= 15) for the whole path to be committed.
+ *   1 <= n_nodes <= 64, 1 <= head_dim <= 1024, ctx_capacity >= 1,
+ *   path_stride >= 1; pointers aligned to their element size.  No workspace.
+ */
+glance_status glance_commit_path(int32_t batch, int32_t n_nodes, int32_t n_kv_heads, int32_t head_dim,
+                                 int32_t ctx_capacity, glance_dtype dtype, const void* k_new,
+                                 const void* v_new, const int32_t* accept_len, const int32_t* accept_path,
+                                 int32_t path_stride, void* k_ctx, void* v_ctx, int32_t* ctx_lens,
+                                 hipStream_t stream);
+
+/*
  * Draft tree builder (Algorithm 1, second step; Sec. 3.3 with the plug-in
  * score of Assumption 1, Sec. 3.2).  From the drafter's logits z_j at offsets
  * j = 1..horizon, q_j = softmax(z_j), keep the `budget` strings y_{1:l}
@@ -237,11 +273,11 @@ const char* glance_status_string(glance_status status);
 const char* glance_last_error(void);
 
 /*
- * Profiling hook.  When both events are non-NULL, the next attention, accept
- * or tree-builder call on this thread records `start` on its stream right
- * before its main kernel (the split-KV attention kernel, the vocabulary
- * argmax kernel, or both passes of the tree builder) and `stop` right after
- * it, then forgets the pair.  Arguments are hipEvent_t handles created by
+ * Profiling hook.  When both events are non-NULL, the next attention, accept,
+ * commit or tree-builder call on this thread records `start` on its stream
+ * right before its main kernel (the split-KV attention kernel, the vocabulary
+ * argmax kernel, the commit kernel, or all passes of the tree builder) and
+ * `stop` right after it, then forgets the pair.  Arguments are hipEvent_t handles created by
  * the caller.  Pass NULLs to clear.
  */
 glance_status glance_set_kernel_events(void* start_event, void* stop_event);

@@ -12,6 +12,7 @@ missing or a GPU is absent, the calls raise.
     glance_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents) -> (out, lse)
     glance_greedy_accept(logits, parents, tokens) -> dict(argmax, accept_len, accept_path, next_root)
     glance_build_tree(draft_logits, roots, budget) -> dict(parents, tokens, scores)
+    glance_commit_path(k_new, v_new, accept_len, accept_path, k_ctx, v_ctx, ctx_lens)  (in place)
 
 Layouts: q, out [batch][n][Hq][D]; k_ctx, v_ctx [batch][Hkv][capacity][D];
 k_new, v_new [batch][n][Hkv][D]; ctx_lens [batch] int32; parents, tokens
@@ -58,6 +59,8 @@ _SIGS = {
     "glance_build_tree": (ctypes.c_int, [_I32, _I32, _I32, _I32, ctypes.c_int, _P, ctypes.c_int64, _P, _P,
                                          _P, _P, _P, _SZ, _P]),
     "glance_tree_workspace_size": (_SZ, [_I32, _I32, _I32, _I32]),
+    "glance_commit_path": (ctypes.c_int, [_I32, _I32, _I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _I32, _P,
+                                          _P, _P, _P]),
     "glance_attn_workspace_size": (_SZ, [ctypes.POINTER(AttnShape)]),
     "glance_accept_workspace_size": (_SZ, [_I32, _I32, _I32]),
     "glance_validate_tree": (ctypes.c_int, [_I32, _P, _P, _I32]),
@@ -333,6 +336,35 @@ def glance_build_tree(draft_logits, roots, budget, first_row=0, horizon=None, ou
                                   want_scores)
     _check(lib().glance_build_tree(*args))
     return outputs
+
+
+def _commit_args(k_new, v_new, accept_len, accept_path, k_ctx, v_ctx, ctx_lens, stream):
+    torch = _torch()
+    _dev(k_new, "k_new", ndim=4)
+    code = _dtype_code(k_new)
+    batch, n, hkv, d = k_new.shape
+    _dev(v_new, "v_new", k_new.dtype, 4)
+    _dev(k_ctx, "k_ctx", k_new.dtype, 4)
+    _dev(v_ctx, "v_ctx", k_new.dtype, 4)
+    cap = k_ctx.shape[2]
+    if tuple(v_new.shape) != tuple(k_new.shape):
+        raise ValueError("v_new must match k_new")
+    if tuple(k_ctx.shape) != (batch, hkv, cap, d) or tuple(v_ctx.shape) != (batch, hkv, cap, d):
+        raise ValueError("k_ctx / v_ctx must be [batch][Hkv][capacity][D] matching k_new")
+    _dev(accept_len, "accept_len", torch.int32, 1)
+    _dev(accept_path, "accept_path", torch.int32, 2)
+    _dev(ctx_lens, "ctx_lens", torch.int32, 1)
+    if accept_len.shape[0] != batch or accept_path.shape[0] != batch or ctx_lens.shape[0] != batch:
+        raise ValueError("accept_len, accept_path and ctx_lens need one row per sequence")
+    return [ctypes.c_int32(batch), ctypes.c_int32(n), ctypes.c_int32(hkv), ctypes.c_int32(d), ctypes.c_int32(cap),
+            ctypes.c_int(code), _ptr(k_new), _ptr(v_new), _ptr(accept_len), _ptr(accept_path),
+            ctypes.c_int32(accept_path.shape[1]), _ptr(k_ctx), _ptr(v_ctx), _ptr(ctx_lens), _stream(stream)]
+
+
+def glance_commit_path(k_new, v_new, accept_len, accept_path, k_ctx, v_ctx, ctx_lens, stream=None):
+    """Append the accepted path's key/value rows to the caches and advance ctx_lens (in place)."""
+    _check(lib().glance_commit_path(*_commit_args(k_new, v_new, accept_len, accept_path, k_ctx, v_ctx,
+                                                  ctx_lens, stream)))
 
 
 # ---------------------------------------------------------------- prepared calls

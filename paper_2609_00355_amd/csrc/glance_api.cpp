@@ -428,6 +428,58 @@ size_t glance_tree_workspace_size(int32_t batch, int32_t horizon, int32_t vocab,
   return pl.bytes;
 }
 
+glance_status glance_commit_path(int32_t batch, int32_t n_nodes, int32_t n_kv_heads, int32_t head_dim,
+                                 int32_t ctx_capacity, glance_dtype dtype, const void* k_new,
+                                 const void* v_new, const int32_t* accept_len, const int32_t* accept_path,
+                                 int32_t path_stride, void* k_ctx, void* v_ctx, int32_t* ctx_lens,
+                                 hipStream_t stream) {
+  if (batch < 1) return fail(GLANCE_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", batch);
+  if (n_nodes < 1 || n_nodes > 64)
+    return fail(GLANCE_ERR_UNSUPPORTED, "n_nodes must be in 1..64 (got %d)", n_nodes);
+  if (n_kv_heads < 1) return fail(GLANCE_ERR_INVALID_ARG, "n_kv_heads must be >= 1");
+  if (head_dim < 1 || head_dim > 1024) return fail(GLANCE_ERR_UNSUPPORTED, "head_dim must be in 1..1024");
+  if (ctx_capacity < 1) return fail(GLANCE_ERR_INVALID_ARG, "ctx_capacity must be >= 1");
+  if (path_stride < 1) return fail(GLANCE_ERR_INVALID_ARG, "path_stride must be >= 1");
+  if (dtype != GLANCE_F32 && dtype != GLANCE_BF16)
+    return fail(GLANCE_ERR_UNSUPPORTED, "dtype must be GLANCE_F32 or GLANCE_BF16");
+  // per-sequence copy index arithmetic stays in 32 bits
+  if ((long long)64 * n_kv_heads * head_dim * 2 > 0x7fffffffLL)
+    return fail(GLANCE_ERR_UNSUPPORTED, "n_kv_heads * head_dim too large");
+  const size_t esz = dtype == GLANCE_BF16 ? 2 : 4;
+  struct {
+    const void* ptr;
+    const char* name;
+    size_t align;
+  } req[] = {{k_new, "k_new", esz},          {v_new, "v_new", esz},           {k_ctx, "k_ctx", esz},
+             {v_ctx, "v_ctx", esz},          {accept_len, "accept_len", 4}, {accept_path, "accept_path", 4},
+             {ctx_lens, "ctx_lens", 4}};
+  for (auto& r : req) {
+    if (!r.ptr) return fail(GLANCE_ERR_INVALID_ARG, "%s is NULL", r.name);
+    if (reinterpret_cast<uintptr_t>(r.ptr) & (r.align - 1))
+      return fail(GLANCE_ERR_INVALID_ARG, "%s is not %zu-byte aligned", r.name, r.align);
+  }
+  glance::CommitParams p = {};
+  p.k_new = k_new;
+  p.v_new = v_new;
+  p.accept_len = accept_len;
+  p.accept_path = accept_path;
+  p.k_ctx = k_ctx;
+  p.v_ctx = v_ctx;
+  p.ctx_lens = ctx_lens;
+  p.batch = batch;
+  p.n = n_nodes;
+  p.hkv = n_kv_heads;
+  p.d = head_dim;
+  p.cap = ctx_capacity;
+  p.path_stride = path_stride;
+  p.esz = (int)esz;
+  p.vec = ((size_t)head_dim * esz) % 16 == 0 && aligned16(k_new) && aligned16(v_new) && aligned16(k_ctx) &&
+          aligned16(v_ctx);
+  hipEvent_t e0, e1;
+  take_events(&e0, &e1);
+  return check_hip(glance::launch_commit(p, stream, e0, e1), "commit kernel launch");
+}
+
 size_t glance_attn_workspace_size(const glance_attn_shape* s) {
   Plan pl;
   if (make_plan(s, &pl) != GLANCE_OK) return 0;
@@ -484,6 +536,6 @@ glance_status glance_set_kernel_events(void* start_event, void* stop_event) {
   return ok();
 }
 
-int32_t glance_version(void) { return 200; }
+int32_t glance_version(void) { return 300; }
 
 }  // extern "C"

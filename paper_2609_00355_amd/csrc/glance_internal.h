@@ -102,10 +102,26 @@ struct TreeParams {
   int vec;          // rows are 16-byte aligned: vector loads
 };
 
+// Commit of an accepted path: k_new/v_new [batch][n][hkv][d] rows of the path
+// nodes into k_ctx/v_ctx [batch][hkv][cap][d] at ctx_lens[b] + i.
+struct CommitParams {
+  const void* k_new;
+  const void* v_new;
+  const int32_t* accept_len;
+  const int32_t* accept_path;
+  void* k_ctx;
+  void* v_ctx;
+  int32_t* ctx_lens;
+  int batch, n, hkv, d, cap, path_stride;
+  int esz;  // bytes per element, 2 or 4
+  int vec;  // rows are 16-byte multiples and every pointer is 16-byte aligned
+};
+
 hipError_t launch_attn_bf16(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_attn_f32(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_attn_merge(const AttnParams& p, bool out_bf16, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_tree(const TreeParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+hipError_t launch_commit(const CommitParams& p, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
 }  // namespace glance

@@ -172,6 +172,33 @@ def test_tree_builder_argument_checks(lib, kw, code, word):
     assert word in G.glance_last_error()
 
 
+def _commit(lib, batch=1, n=64, hkv=4, d=128, cap=4096, dtype=G.GLANCE_BF16, k_new=FAKE, v_new=FAKE,
+            alen=FAKE, apath=FAKE, stride=16, k_ctx=FAKE, v_ctx=FAKE, lens=FAKE):
+    return lib.glance_commit_path(batch, n, hkv, d, cap, dtype, k_new, v_new, alen, apath, stride, k_ctx, v_ctx,
+                                  lens, None)
+
+
+@pytest.mark.parametrize("kw,code,word", [
+    (dict(batch=0), G.GLANCE_ERR_INVALID_ARG, "batch"),
+    (dict(n=0), G.GLANCE_ERR_UNSUPPORTED, "n_nodes"),
+    (dict(n=65), G.GLANCE_ERR_UNSUPPORTED, "n_nodes"),
+    (dict(hkv=0), G.GLANCE_ERR_INVALID_ARG, "n_kv_heads"),
+    (dict(d=0), G.GLANCE_ERR_UNSUPPORTED, "head_dim"),
+    (dict(d=2048), G.GLANCE_ERR_UNSUPPORTED, "head_dim"),
+    (dict(cap=0), G.GLANCE_ERR_INVALID_ARG, "ctx_capacity"),
+    (dict(stride=0), G.GLANCE_ERR_INVALID_ARG, "path_stride"),
+    (dict(dtype=7), G.GLANCE_ERR_UNSUPPORTED, "dtype"),
+    (dict(k_new=None), G.GLANCE_ERR_INVALID_ARG, "k_new"),
+    (dict(v_ctx=None), G.GLANCE_ERR_INVALID_ARG, "v_ctx"),
+    (dict(lens=None), G.GLANCE_ERR_INVALID_ARG, "ctx_lens"),
+    (dict(k_ctx=ctypes.c_void_p(0x10001)), G.GLANCE_ERR_INVALID_ARG, "aligned"),
+    (dict(apath=ctypes.c_void_p(0x10002)), G.GLANCE_ERR_INVALID_ARG, "accept_path"),
+])
+def test_commit_argument_checks(lib, kw, code, word):
+    assert _commit(lib, **kw) == code
+    assert word in G.glance_last_error()
+
+
 @pytest.mark.parametrize("parents,tokens,max_depth,ok", [
     ([-1], None, 15, True),
     ([-1, 0, 0, 1, 3], [9, 1, 2, 3, 4], 15, True),
