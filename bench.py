@@ -264,6 +264,38 @@ def measure_tree_builder(args, w, G, C, torch, np, dev, stream):
             "traffic": traffic, "tree_depth": depth}
 
 
+def measure_commit(args, w, s, G, torch, np, dev, stream, ctx):
+    """The commit of the round's accepted paths (root + accepted nodes' keys and
+    values of the verify pass appended to a cache with room for them), timed
+    with HIP events around its kernel; the lengths are reset between calls
+    outside the timed interval."""
+    vv = s["keep"][1]
+    k_new, v_new = vv["k_new"], vv["v_new"]
+    a_out = s["a_out"]
+    cap = int(max(ctx)) + w.n_tree
+    k_ctx = torch.zeros((w.batch, w.hkv, cap, w.d), dtype=k_new.dtype, device=dev)
+    v_ctx = torch.zeros_like(k_ctx)
+    lens0 = torch.as_tensor(np.asarray(ctx, dtype=np.int32)).to(dev)
+    lens = lens0.clone()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, b in evs:
+        a.record(stream)
+        b.record(stream)
+    for i in range(args.warmup + args.steps):
+        lens.copy_(lens0)
+        if i >= args.warmup:
+            G.glance_set_kernel_events(*evs[i - args.warmup])
+        G.glance_commit_path(k_new, v_new, a_out["accept_len"], a_out["accept_path"], k_ctx, v_ctx, lens,
+                             stream=stream)
+    torch.cuda.synchronize()
+    us = float(np.median([a.elapsed_time(b) for a, b in evs]) * 1e3)
+    rows = int((a_out["accept_len"].cpu().numpy() + 1).sum())
+    nbytes = rows * w.hkv * w.d * k_new.element_size() * 2 * 2  # K and V, read and written
+    return {"us": round(us, 2), "kernel": "commit_kernel", "rows": rows, "bytes": nbytes,
+            "bound": "launch latency (a few KB per call)"}
+
+
 def main():
     args = parse()
     if args.traffic_from:
@@ -424,6 +456,7 @@ def main():
     roof["kernel"] = per_kernel[dom]["kernel"]
 
     tree = None if args.no_tree else measure_tree_builder(args, w, G, C, torch, np, dev, stream)
+    commit = measure_commit(args, w, sets[0], G, torch, np, dev, stream, ctx)
 
     acc = sets[0]["a_out"]["accept_len"].cpu().numpy()
     res = {
@@ -455,6 +488,7 @@ def main():
     }
     if tree is not None:
         res["tree_builder"] = tree
+    res["commit"] = commit
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(inputs, args.cpu_seconds)
     print(json.dumps(res), flush=True)

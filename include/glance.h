@@ -158,6 +158,12 @@ glance_status glance_tree_verify_attn(const glance_attn_shape* s, const void* q,
  *   next_root   device [batch] int32: the bonus token argmax_out[b][last node],
  *               which the round commits after the a accepted tokens and which
  *               becomes the next round's root.
+ *   root_entropy device [batch] float32, or NULL: the entropy (nats) of the
+ *               softmax of row 0, the target's next-token distribution at the
+ *               round root -- the scalar the paper's entropy law (Sec. 4)
+ *               predicts acceptance from.  Computed in the argmax pass (fp32
+ *               sums relative to each chunk's maximum); -inf logits carry
+ *               probability 0; undefined if row 0 holds a NaN or +inf.
  * Walk: v = 0; t = argmax(row v); if some child c of v has tokens[c] == t
  * (lowest such c if siblings repeat a token), append c and continue from c,
  * else stop.  Each step moves to a larger node index, so the walk ends within
@@ -168,8 +174,8 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    glance_dtype logits_dtype, const void* logits,
                                    const int32_t* parents, const int32_t* tokens,
                                    int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
-                                   int32_t path_stride, int32_t* next_root, void* workspace,
-                                   size_t workspace_bytes, hipStream_t stream);
+                                   int32_t path_stride, int32_t* next_root, float* root_entropy,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Commit of a round's accepted path into a context cache (the walk of Def. 1

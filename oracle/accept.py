@@ -16,6 +16,10 @@ TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
   the root and checks that every edge carries the argmax token of the parent
   row; the answer is the deepest such node.
 
+* ``row_entropy``  -- H = -sum_w p(w) log p(w) of p = softmax(row), in nats: the
+  target's next-token entropy, which the paper's entropy law (Sec. 4) reads at
+  the round root (row 0).  -inf logits carry probability 0.
+
 A round commits a + 1 tokens: the a accepted tree tokens and the bonus token
 read off the last verified row (Sec. 3.1, Eq. 1).
 """
@@ -121,3 +125,19 @@ def greedy_accept(logits, parents, tokens, path_stride=None):
         committed.append([int(tokens[b][c]) for c in path[1:]] + [int(nr)])
     return {"argmax": am, "accept_len": acc, "accept_path": paths, "next_root": roots,
             "committed": committed}
+
+
+def row_entropy(row):
+    """Entropy in nats of softmax(row) for one row of logits (float64)."""
+    if hasattr(row, "detach"):
+        t = row.detach().to("cpu")
+        if str(t.dtype) in ("torch.bfloat16", "torch.float16"):
+            t = t.float()
+        row = t.numpy()
+    z = np.asarray(row, dtype=np.float64)
+    z = z[np.isfinite(z)]
+    m = z.max()
+    e = np.exp(z - m)
+    s = e.sum()
+    p = e / s
+    return float(-(p * ((z - m) - np.log(s))).sum())

@@ -55,7 +55,7 @@ _SIGS = {
     "glance_tree_verify_attn": (ctypes.c_int, [ctypes.POINTER(AttnShape), _P, _P, _P, _P, _P, _P, _P, _P,
                                                _P, _P, _SZ, _P]),
     "glance_greedy_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P, _P, _I32,
-                                            _P, _P, _SZ, _P]),
+                                            _P, _P, _P, _SZ, _P]),
     "glance_build_tree": (ctypes.c_int, [_I32, _I32, _I32, _I32, ctypes.c_int, _P, ctypes.c_int64, _P, _P,
                                          _P, _P, _P, _SZ, _P]),
     "glance_tree_workspace_size": (_SZ, [_I32, _I32, _I32, _I32]),
@@ -252,8 +252,16 @@ def glance_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, ou
 
 
 def glance_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None, workspace=None,
-                         stream=None):
-    """Row argmax + the walk of Algorithm 1.  Returns a dict of int32 GPU tensors."""
+                         stream=None, want_entropy=False):
+    """Row argmax + the walk of Algorithm 1.  Returns a dict of GPU tensors (int32, and
+    float32 root_entropy [batch] when want_entropy)."""
+    args, outputs, _ = _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream,
+                                    want_entropy)
+    _check(lib().glance_greedy_accept(*args))
+    return outputs
+
+
+def _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream, want_entropy):
     torch = _torch()
     _dev(logits, "logits", ndim=3)
     code = _dtype_code(logits)
@@ -271,17 +279,18 @@ def glance_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None
             "accept_path": torch.empty((batch, path_stride), dtype=torch.int32, device=dev),
             "next_root": torch.empty((batch,), dtype=torch.int32, device=dev),
         }
+    if want_entropy and outputs.get("root_entropy") is None:
+        outputs["root_entropy"] = torch.empty((batch,), dtype=torch.float32, device=dev)
     need = glance_accept_workspace_size(batch, n, vocab)
     if need == 0:
         raise GlanceError(GLANCE_ERR_INVALID_ARG, glance_last_error())
     ws = _workspace(need, dev, workspace)
-    st = lib().glance_greedy_accept(batch, n, vocab, code, _ptr(logits), _ptr(parents), _ptr(tokens),
-                                    _ptr(outputs["argmax"]), _ptr(outputs["accept_len"]),
-                                    _ptr(outputs["accept_path"]), path_stride,
-                                    _ptr(outputs["next_root"]), _ptr(ws),
-                                    ws.numel() * ws.element_size(), _stream(stream))
-    _check(st)
-    return outputs
+    args = [ctypes.c_int32(batch), ctypes.c_int32(n), ctypes.c_int32(vocab), ctypes.c_int(code), _ptr(logits),
+            _ptr(parents), _ptr(tokens), _ptr(outputs["argmax"]), _ptr(outputs["accept_len"]),
+            _ptr(outputs["accept_path"]), ctypes.c_int32(path_stride), _ptr(outputs["next_root"]),
+            _ptr(outputs.get("root_entropy")), _ptr(ws), ctypes.c_size_t(ws.numel() * ws.element_size()),
+            _stream(stream)]
+    return args, outputs, ws
 
 
 def _tree_args(draft_logits, roots, budget, first_row, horizon, outputs, workspace, stream, want_scores):
@@ -425,16 +434,11 @@ def prepare_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, o
 
 
 def prepare_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None, workspace=None,
-                          stream=None):
+                          stream=None, want_entropy=False):
     """Returns (call, outputs): call() re-runs the acceptance into the outputs dict."""
-    batch, n, vocab = logits.shape
-    ws = _workspace(glance_accept_workspace_size(batch, n, vocab), logits.device, workspace)
-    outputs = glance_greedy_accept(logits, parents, tokens, path_stride, outputs, ws, stream)
-    path_stride = int(path_stride or n)
-    args = [ctypes.c_int32(batch), ctypes.c_int32(n), ctypes.c_int32(vocab), ctypes.c_int(_dtype_code(logits)),
-            _ptr(logits), _ptr(parents), _ptr(tokens), _ptr(outputs["argmax"]), _ptr(outputs["accept_len"]),
-            _ptr(outputs["accept_path"]), ctypes.c_int32(path_stride), _ptr(outputs["next_root"]), _ptr(ws),
-            ctypes.c_size_t(ws.numel() * ws.element_size()), _stream(stream)]
+    args, outputs, ws = _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream,
+                                     want_entropy)
+    _check(lib().glance_greedy_accept(*args))
     keep = (logits, parents, tokens, outputs, ws)
     return PreparedCall(lib().glance_greedy_accept, args, keep), outputs
 

@@ -10,6 +10,13 @@
 //                 child that carries the current row's argmax token with one
 //                 ballot per step.
 //
+// Root entropy (optional): the target's next-token entropy at the round root,
+// H = -sum_w p(w) log p(w) over row 0 of each sequence (the scalar of the
+// paper's entropy law, Sec. 4).  The argmax workgroups of row 0 re-read their
+// chunk (1/n_nodes of the logits) to accumulate, relative to the chunk
+// maximum m found by the argmax, S = sum e^(z - m) and T = sum e^(z - m) (z - m);
+// the walk merges the chunks to H = log S - T / S.
+//
 // Order key of a float (fp32 bits, or bf16 bits shifted up 16): the sign-
 // magnitude encoding mapped to two's complement, so +0 and -0 both map to 0
 // (they tie, and the lowest index wins), and every NaN maps to INT32_MAX (a
@@ -32,6 +39,12 @@ __device__ __forceinline__ int order_key(unsigned int bits) {
 __device__ __forceinline__ unsigned long long pack(int key, int idx) {
   return ((unsigned long long)((unsigned int)key ^ 0x80000000u) << 32) |
          (unsigned long long)(0xffffffffu - (unsigned int)idx);
+}
+
+// Inverse of order_key for a non-NaN key: the fp32 bits of the value.
+__device__ __forceinline__ float key_to_float(int key) {
+  const unsigned bits = key >= 0 ? (unsigned)key : 0x80000000u - (unsigned)key;
+  return __builtin_bit_cast(float, bits);
 }
 
 __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
@@ -164,9 +177,42 @@ __global__ __launch_bounds__(256) void argmax_partial(AcceptParams p) {
   w = wave_max64(w);
   if ((tid & 63) == 0) red[tid >> 6] = w;
   __syncthreads();
+  __shared__ float ent[2][4];
+  __shared__ float s_m;
   if (tid == 0) {
     const unsigned long long r = umax64(umax64(red[0], red[1]), umax64(red[2], red[3]));
     p.part[row * p.chunks + chunk] = r;
+    s_m = key_to_float((int)((unsigned)(r >> 32) ^ 0x80000000u));
+  }
+  if (p.root_entropy == nullptr || row % p.n_nodes != 0) return;
+  // root row: entropy statistics of the chunk relative to its maximum
+  __syncthreads();
+  const float m = s_m;
+  float S = 0.f, T = 0.f;
+  for (int e = c0 + tid; e < c1; e += 256) {
+    const float z = BF16 ? __builtin_bit_cast(float, (unsigned)static_cast<const unsigned short*>(p.logits)[row * (long)p.vocab + e] << 16)
+                         : static_cast<const float*>(p.logits)[row * (long)p.vocab + e];
+    if (z != -__builtin_inff()) {
+      const float d = z - m;
+      const float x = __builtin_amdgcn_exp2f(d * 1.4426950408889634f);
+      S += x;
+      T += x * d;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    S += __shfl_xor(S, off);
+    T += __shfl_xor(T, off);
+  }
+  if ((tid & 63) == 0) {
+    ent[0][tid >> 6] = S;
+    ent[1][tid >> 6] = T;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const float s_all = (ent[0][0] + ent[0][1]) + (ent[0][2] + ent[0][3]);
+    const float t_all = (ent[1][0] + ent[1][1]) + (ent[1][2] + ent[1][3]);
+    p.ent_part[(row / p.n_nodes) * p.chunks + chunk] = make_float4(m, s_all, t_all, 0.f);
   }
 }
 
@@ -211,6 +257,22 @@ __global__ __launch_bounds__(64) void accept_walk(AcceptParams p) {
   if (lane == 0) {
     p.accept_len[b] = len;
     p.next_root[b] = sAm[v];
+  }
+  if (p.root_entropy && lane == 0) {
+    // merge the chunks relative to the row maximum M:
+    // e^(z-M) (z-M) = e^(m-M) e^(z-m) ((z-m) + (m-M))
+    const float4* ep = p.ent_part + (long)b * p.chunks;
+    float M = -__builtin_inff();
+    for (int c = 0; c < p.chunks; ++c) M = fmaxf(M, ep[c].x);
+    float S = 0.f, T = 0.f;
+    for (int c = 0; c < p.chunks; ++c) {
+      const float4 q = ep[c];
+      if (q.y == 0.f) continue;  // a chunk of -inf logits holds no mass
+      const float f = __builtin_amdgcn_exp2f((q.x - M) * 1.4426950408889634f);
+      S += q.y * f;
+      T += (q.z + (q.x - M) * q.y) * f;
+    }
+    p.root_entropy[b] = __builtin_amdgcn_logf(S) * 0.6931471805599453f - T / S;
   }
 }
 

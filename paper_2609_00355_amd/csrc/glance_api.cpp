@@ -199,7 +199,7 @@ glance_status attn_common(bool tree, const glance_attn_shape* s, const void* q, 
 
 struct AcceptPlan {
   int chunks, chunk_len;
-  size_t bytes;
+  size_t part_bytes, bytes;
 };
 
 glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptPlan* out) {
@@ -224,7 +224,8 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
   chunks = ((long long)vocab + len - 1) / len;
   out->chunks = (int)chunks;
   out->chunk_len = (int)len;
-  out->bytes = round_up((size_t)rows * chunks * sizeof(unsigned long long), 256);
+  out->part_bytes = round_up((size_t)rows * chunks * sizeof(unsigned long long), 256);
+  out->bytes = out->part_bytes + round_up((size_t)batch * chunks * sizeof(float4), 256);
   return ok();
 }
 
@@ -321,8 +322,8 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    glance_dtype logits_dtype, const void* logits,
                                    const int32_t* parents, const int32_t* tokens,
                                    int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
-                                   int32_t path_stride, int32_t* next_root, void* workspace,
-                                   size_t workspace_bytes, hipStream_t stream) {
+                                   int32_t path_stride, int32_t* next_root, float* root_entropy,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
   AcceptPlan pl;
   glance_status st = accept_plan(batch, n_nodes, vocab, &pl);
   if (st != GLANCE_OK) return st;
@@ -341,6 +342,8 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
   }
   if (logits_dtype == GLANCE_BF16 && (reinterpret_cast<uintptr_t>(logits) & 1u))
     return fail(GLANCE_ERR_INVALID_ARG, "logits is not 2-byte aligned");
+  if (root_entropy && (reinterpret_cast<uintptr_t>(root_entropy) & 3u))
+    return fail(GLANCE_ERR_INVALID_ARG, "root_entropy is not 4-byte aligned");
   if (!workspace) return fail(GLANCE_ERR_WORKSPACE, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(GLANCE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
@@ -355,7 +358,9 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
   p.accept_len = accept_len;
   p.accept_path = accept_path;
   p.next_root = next_root;
+  p.root_entropy = root_entropy;
   p.part = static_cast<unsigned long long*>(workspace);
+  p.ent_part = reinterpret_cast<float4*>(static_cast<char*>(workspace) + pl.part_bytes);
   p.batch = batch;
   p.n_nodes = n_nodes;
   p.vocab = vocab;

@@ -57,7 +57,9 @@ struct AcceptParams {
   int32_t* accept_len;
   int32_t* accept_path;
   int32_t* next_root;
+  float* root_entropy;       // [batch] or null: entropy of each sequence's row 0
   unsigned long long* part;  // [batch * n_nodes][chunks] packed (key, ~index)
+  float4* ent_part;          // [batch][chunks] (chunk max m, sum e^(z-m), sum e^(z-m) (z-m), 0)
   int batch, n_nodes, vocab, path_stride;
   int chunks, chunk_len;     // chunk_len is a multiple of 8
 };

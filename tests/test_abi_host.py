@@ -115,16 +115,16 @@ def test_accept_argument_checks(lib):
     assert G.glance_accept_workspace_size(0, 64, 10) == 0
     assert G.glance_accept_workspace_size(1, 65, 10) == 0
     st = lib.glance_greedy_accept(1, 65, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16, FAKE,
-                                  FAKE, 1 << 20, None)
+                                  None, FAKE, 1 << 20, None)
     assert st == G.GLANCE_ERR_UNSUPPORTED
     st = lib.glance_greedy_accept(1, 8, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, FAKE,
-                                  FAKE, 1 << 20, None)
+                                  None, FAKE, 1 << 20, None)
     assert st == G.GLANCE_ERR_INVALID_ARG and "path_stride" in G.glance_last_error()
     st = lib.glance_greedy_accept(1, 8, 100, G.GLANCE_BF16, FAKE, None, FAKE, FAKE, FAKE, FAKE, 8, FAKE,
-                                  FAKE, 1 << 20, None)
+                                  None, FAKE, 1 << 20, None)
     assert st == G.GLANCE_ERR_INVALID_ARG and "parents" in G.glance_last_error()
     st = lib.glance_greedy_accept(1, 8, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8, FAKE,
-                                  FAKE, 1, None)
+                                  None, FAKE, 1, None)
     assert st == G.GLANCE_ERR_WORKSPACE
 
 

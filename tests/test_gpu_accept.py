@@ -1,12 +1,15 @@
 """Bit-exact parity of the HIP greedy acceptance with the oracle: argmax of
 every row (lowest index on ties), accepted length, accepted path and the
-bonus token, on planted logits, tie fixtures and edge cases."""
+bonus token, on planted logits, tie fixtures and edge cases; the optional root
+entropy within fp32 rounding of the float64 definition."""
 
 import numpy as np
 import pytest
 import torch
 
+import paper_2609_00355_amd as G
 from gpu_helpers import assert_accept_equal, ensure_lib, run_accept
+from oracle import accept as OA
 from workloads import configs as C
 
 pytestmark = pytest.mark.gpu
@@ -189,3 +192,33 @@ def test_many_sequences():
     logits = C.planted_logits(w, par, tok, 6)
     got = run_accept(logits, par, tok, path_stride=16)
     assert_accept_equal(got, logits, par, tok, path_stride=16)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("case", ["planted", "uniform", "masked", "small_vocab"])
+def test_root_entropy(dtype, case):
+    """Entropy of each sequence's row 0 (fused into the argmax pass) against float64."""
+    w = C.WORKLOADS["verify_4k"]
+    batch, n = 3, 8
+    par, tok = C.tree_inputs(w, seed=5, batch=batch, n=n)
+    vocab = 7 if case == "small_vocab" else w.vocab
+    g = torch.Generator().manual_seed(11)
+    logits = (torch.randn(batch, n, vocab, generator=g) * 1.4).to(dtype)
+    if case == "planted":
+        logits[:, 0, 5] = 14.0          # a confident root row
+    elif case == "uniform":
+        logits[:, 0] = 0.5
+    elif case == "masked":
+        logits[:, 0, 1000:] = float("-inf")
+    tok = tok % vocab
+    res = G.glance_greedy_accept(logits.cuda(), par.cuda(), tok.cuda(), want_entropy=True)
+    h = res["root_entropy"].cpu().numpy()
+    for b in range(batch):
+        ref = OA.row_entropy(logits[b, 0])
+        assert abs(h[b] - ref) <= 2e-4 + 2e-5 * abs(ref), (b, h[b], ref)
+    if case == "uniform":
+        assert abs(h[0] - np.log(vocab)) < 2e-4 + 2e-5 * np.log(vocab)
+    # the argmax and walk are unchanged by the extra output
+    plain = G.glance_greedy_accept(logits.cuda(), par.cuda(), tok.cuda())
+    for k in ("argmax", "accept_len", "accept_path", "next_root"):
+        assert torch.equal(plain[k], res[k])

@@ -114,3 +114,23 @@ def test_batched_accept_padding_and_outputs():
     assert res["accept_path"].tolist() == [[0, 1, 3, -1, -1], [0, -1, -1, -1, -1]]
     assert res["next_root"].tolist() == [2, 9]
     assert res["argmax"].tolist() == [[5, 7, 0, 2], [9, 0, 0, 0]]
+
+
+# ---------------------------------------------------------------- root entropy
+def test_entropy_closed_forms():
+    assert abs(C.row_entropy(np.zeros(1000)) - np.log(1000)) < 1e-12          # uniform: log V
+    row = np.full(50, -np.inf)
+    row[[3, 40]] = 7.0
+    assert abs(C.row_entropy(row) - np.log(2)) < 1e-12                         # two equal masses
+    row = np.log(np.array([0.5, 0.25, 0.25])) + 3.0
+    assert abs(C.row_entropy(row) - 1.5 * np.log(2)) < 1e-12                   # p = 1/2, 1/4, 1/4
+    row = np.array([0.0, -1e4, -1e4])
+    assert C.row_entropy(row) < 1e-300 + 1e-12                                 # nearly one-hot
+
+
+def test_entropy_is_shift_invariant_and_bounded():
+    rng = np.random.default_rng(2)
+    row = rng.normal(0, 2, size=5000)
+    h = C.row_entropy(row)
+    assert abs(C.row_entropy(row + 123.0) - h) < 1e-9
+    assert 0.0 < h < np.log(5000)
