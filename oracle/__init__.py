@@ -17,6 +17,8 @@ the GPU path:
 * ``commit``     -- the commit of a round's accepted path: the keys and values of
   the root and the accepted nodes join the context cache (Def. 1's walk
   commits them; Eq. 1);
+* ``sampling``   -- the walk at temperature T > 0: each visited row's draw by the
+  Gumbel-max rule with Philox4x32-10 uniforms and a fixed fp32 logarithm;
 * ``tree``       -- the tree builder of Sec. 3.3 (Algorithm 1, second step): the
   N strings of highest plug-in score prod_j q_j(y_j) (Assumption 1) packed as
   a prefix-closed tree, by exhaustive and by best-first enumeration;
@@ -24,4 +26,4 @@ the GPU path:
   lossless greedy equivalence of Thm. 1 (Sec. 3.3, App. A.1).
 """
 
-from . import attention, accept, commit, tiny_model, tree  # noqa: F401
+from . import attention, accept, commit, sampling, tiny_model, tree  # noqa: F401
