@@ -19,13 +19,18 @@ Readings (also listed in the design notes):
   Moraes, Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC'11),
   written here from its definition: key (seed_lo, seed_hi), counter
   (w // 4, node, sequence, round), word w % 4 of the output;
-  u = ((x >> 8) + 0.5) * 2^-24, which is exact in fp32 and never 0 or 1.
+  u = ((x >> 9) + 0.5) * 2^-23: 23 bits, so that k + 0.5 still fits fp32's
+  24-bit significand; u is then exact and lies in [2^-24, 1 - 2^-24].
 * The logarithms are computed by one fixed fp32 recipe that the GPU repeats
   operation for operation (IEEE-rounded +, -, *, /, no fused multiply-add):
-  ln t = e ln 2 + 2 atanh(s), t = m 2^e with m in [1, 2), s = (m - 1) / (m + 1),
-  atanh(s) = s (1 + s^2/3 + s^4/5 + ... + s^14/15).  Both sides then draw the
-  same tokens bit for bit.  The recipe's error against ln is below 3e-7
-  relative (pinned in the tests), far inside what a sampler can show.
+  ln t = e ln 2 + 2 atanh(s), t = m 2^e with m in [sqrt(1/2), sqrt(2)),
+  s = (m - 1) / (m + 1), atanh(s) = s (1 + s^2/3 + s^4/5 + s^6/7 + s^8/9).
+  With that range m - 1 is exact and t near 1 keeps e = 0, so the relative
+  error stays a few ulp even as t -> 1; the Gumbel transform needs exactly
+  that, since -ln u -> 0 as u -> 1.  Both sides then draw the same tokens bit
+  for bit.  The recipe's error against ln is below 3e-7 relative and the
+  Gumbel noise is within 2e-6 of -ln(-ln u) for every one of the 2^23
+  uniforms (both pinned in the tests), far inside what a sampler can show.
 * z / T is one IEEE fp32 division (bf16 logits are widened exactly first).
 """
 
@@ -67,11 +72,12 @@ def uniforms(seed, round_, seq, node, vocab):
     key[:, 0] = np.uint32(seed & 0xFFFFFFFF)
     key[:, 1] = np.uint32((seed >> 32) & 0xFFFFFFFF)
     x = philox4x32_10(ctr, key)[np.arange(vocab), (w & np.uint64(3)).astype(np.int64)]
-    return ((x >> np.uint32(8)).astype(np.float32) + np.float32(0.5)) * np.float32(2.0 ** -24)
+    return ((x >> np.uint32(9)).astype(np.float32) + np.float32(0.5)) * np.float32(2.0 ** -23)
 
 
 _LN2 = np.float32(0.6931471805599453)
-_ODD = [np.float32(1.0 / k) for k in (15, 13, 11, 9, 7, 5, 3)]
+_ODD = [np.float32(1.0 / k) for k in (9, 7, 5, 3)]
+_SQRT2_MANT = np.uint32(0x3504F3)   # mantissa field of sqrt(2) rounded down
 
 
 def ln_f32(t):
@@ -79,7 +85,10 @@ def ln_f32(t):
     t = np.asarray(t, dtype=np.float32)
     bits = t.view(np.uint32)
     e = ((bits >> np.uint32(23)) & np.uint32(0xFF)).astype(np.int32) - 127
-    m = ((bits & np.uint32(0x007FFFFF)) | np.uint32(0x3F800000)).view(np.float32)
+    mant = bits & np.uint32(0x007FFFFF)
+    high = mant > _SQRT2_MANT           # m >= sqrt(2): halve m, so m in [sqrt(1/2), sqrt(2))
+    e = e + high.astype(np.int32)
+    m = (mant | np.where(high, np.uint32(0x3F000000), np.uint32(0x3F800000))).view(np.float32)
     s = (m - np.float32(1.0)) / (m + np.float32(1.0))
     s2 = s * s
     acc = _ODD[0]

@@ -30,18 +30,42 @@ def test_philox_known_answers():
 def test_uniforms_are_open_interval_and_uniform():
     u = S.uniforms(seed=12345, round_=3, seq=1, node=2, vocab=200000)
     assert u.dtype == np.float32 and u.min() > 0 and u.max() < 1
+    # every value the mapping can take is exact, inside (0, 1) and distinct
+    k = np.arange(2 ** 23, dtype=np.uint32)
+    uk = (k.astype(np.float32) + np.float32(0.5)) * np.float32(2.0 ** -23)
+    assert np.array_equal(uk.astype(np.float64), (k.astype(np.float64) + 0.5) / 2.0 ** 23)
+    assert uk[0] == 2.0 ** -24 and uk[-1] == 1 - 2.0 ** -24
     assert stats.kstest(u.astype(np.float64), "uniform").pvalue > 1e-3
     assert not np.array_equal(u, S.uniforms(seed=12345, round_=4, seq=1, node=2, vocab=200000))
 
 
 def test_fixed_logarithm_matches_ln():
-    t = np.concatenate([np.float32(2.0) ** np.arange(-30, 20, dtype=np.float32),
-                        np.random.default_rng(0).uniform(1e-8, 30.0, 100000).astype(np.float32)])
+    one = np.float32(1.0)
+    near_one = np.concatenate([one - np.arange(1, 5000, dtype=np.float32) * np.float32(2.0 ** -24),
+                               one + np.arange(1, 5000, dtype=np.float32) * np.float32(2.0 ** -23)])
+    sqrt2 = np.float32(np.sqrt(2.0))
+    around_sqrt2 = np.nextafter(sqrt2, np.float32(np.inf)) * np.float32(2.0) ** np.arange(-3, 3, dtype=np.float32)
+    t = np.concatenate([np.float32(2.0) ** np.arange(-126, 127, dtype=np.float32),
+                        np.random.default_rng(0).uniform(1e-8, 30.0, 100000).astype(np.float32),
+                        near_one, around_sqrt2, sqrt2 * np.float32(2.0) ** np.arange(-3, 3, dtype=np.float32),
+                        np.array([np.finfo(np.float32).tiny, np.finfo(np.float32).max], np.float32)])
     ref = np.log(t.astype(np.float64))
     got = S.ln_f32(t).astype(np.float64)
-    err = np.abs(got - ref) / np.maximum(np.abs(ref), 1.0)
+    err = np.abs(got - ref) / np.where(ref == 0, 1.0, np.abs(ref))   # relative, also as t -> 1
     assert err.max() < 3e-7
     assert S.ln_f32(np.float32(1.0)) == 0.0
+
+
+def test_gumbel_noise_is_accurate_for_every_uniform():
+    """All 2^23 uniforms the generator can produce: the fixed-recipe Gumbel
+    value is within 2e-6 of -ln(-ln u) (the largest u = 1 - 2^-24 gives
+    ln 2^24 - ..., about 16.64; the smallest u = 2^-24 about -2.81)."""
+    k = np.arange(2 ** 23, dtype=np.uint32)
+    u = (k.astype(np.float32) + np.float32(0.5)) * np.float32(2.0 ** -23)
+    g = S.gumbel(u).astype(np.float64)
+    ref = -np.log(-np.log(u.astype(np.float64)))
+    assert np.abs(g - ref).max() < 2e-6
+    assert abs(g[-1] - (-np.log(-np.log1p(-2.0 ** -24)))) < 1e-5 and abs(g[0] + np.log(24 * np.log(2))) < 1e-5
 
 
 def test_gumbel_moments():
@@ -126,3 +150,19 @@ def test_sampling_walk_preserves_the_target_distribution():
     exp.append(rest_e)
     assert len(obs) >= 8
     assert stats.chisquare(obs, np.array(exp) * sum(obs) / sum(exp)).pvalue > 1e-3
+
+
+def test_gumbel_bound_by_leading_zeros():
+    """g(u) <= -ln(1 - u) <= (clz(r) - 8) ln 2 with r = 2^23 - 1 - k for the
+    uniform u = (k + 0.5) 2^-23 (since -ln u >= 1 - u and 1 - u >= r 2^-23):
+    an upper bound on the noise from the integer alone, which lets a sampler
+    skip the logarithms of tokens that cannot win.  Checked for every k on the
+    fixed recipe's values, with 2^-16 to spare for its rounding."""
+    k = np.arange(2 ** 23, dtype=np.uint32)
+    u = (k.astype(np.float32) + np.float32(0.5)) * np.float32(2.0 ** -23)
+    g = S.gumbel(u).astype(np.float64)
+    r = (np.uint32(0x7FFFFF) - k).astype(np.int64)
+    clz = np.full(r.shape, 32, dtype=np.int64)
+    nz = r > 0
+    clz[nz] = 31 - np.floor(np.log2(r[nz].astype(np.float64))).astype(np.int64)
+    assert np.all(g <= (clz - 8) * np.log(2.0) + 2.0 ** -16)
