@@ -17,6 +17,9 @@
  *                            walk of Algorithm 1: the longest root-to-node path
  *                            whose every edge carries the parent row's argmax,
  *                            plus the bonus token that becomes the next root;
+ *   glance_sample_accept     the same walk under sampling at temperature T:
+ *                            each row's token is a Gumbel-max draw from
+ *                            softmax(z / T) with counter-based noise;
  *   glance_commit_path       the commit of a round: the keys and values of the
  *                            root and the accepted nodes join the context
  *                            cache, whose length advances (Def. 1, Eq. 1);
@@ -176,6 +179,46 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
                                    int32_t path_stride, int32_t* next_root, float* root_entropy,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Sampling acceptance at temperature T > 0 (the Limitations section: under
+ * sampling the walk draws a token from the verified row of its node and
+ * descends while the draw is a child in the tree, so every committed token
+ * is a draw from the target's own distribution; the Sampling paragraph of
+ * the Implementation Details appendix runs this at T = 1).
+ * Every row v of sequence b gets one draw from softmax(z / T) by the
+ * Gumbel-max rule:  draw = argmax_w  z_w / T + g_w,  g_w = -ln(-ln u_w),
+ * lowest index on ties, where
+ *   u_w = ((x >> 9) + 0.5) * 2^-23  and  x = word (w mod 4) of
+ *   Philox4x32-10(counter = (w / 4, v, b, round), key = (seed low 32 bits,
+ *   seed high 32 bits))   (Salmon et al., SC'11),
+ * and both logarithms use one fixed fp32 recipe (t = m 2^e with m in
+ * [sqrt(1/2), sqrt(2)), then e ln 2 + 2 s (1 + s^2/3 + s^4/5 + s^6/7 + s^8/9),
+ * s = (m - 1) / (m + 1); IEEE-rounded operations without fused multiply-add;
+ * z / T is one IEEE division, bf16 logits widened exactly).  The draws are
+ * therefore a pure function of (logits, T, seed, round, b, v), reproducible
+ * bit for bit on any IEEE machine.  The walk is glance_greedy_accept's with
+ * the draws in place of the argmax: from v = 0, descend to the lowest child
+ * c of v whose token equals draw(v); next_root is the draw of the last node.
+ * The draws of rows the walk does not visit are returned but unused.
+ *
+ *   temperature  finite, >= 2^-126 (a normal float); T = 0 is
+ *                glance_greedy_accept
+ *   seed, round  the generator's key and the round number (callers advance
+ *                round every round so that draws never repeat)
+ *   draws_out    device [batch][n_nodes] int32: each row's draw
+ *   other arguments, shapes, output layouts and the workspace: as for
+ *   glance_greedy_accept (glance_accept_workspace_size); no root entropy.
+ * NaN logits count as larger than every number (the first NaN wins); -inf
+ * is a token of probability 0.
+ */
+glance_status glance_sample_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                   glance_dtype logits_dtype, const void* logits,
+                                   const int32_t* parents, const int32_t* tokens, float temperature,
+                                   uint64_t seed, uint32_t round, int32_t* draws_out,
+                                   int32_t* accept_len, int32_t* accept_path, int32_t path_stride,
+                                   int32_t* next_root, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
 
 /*
  * Commit of a round's accepted path into a context cache (the walk of Def. 1

@@ -11,6 +11,8 @@ missing or a GPU is absent, the calls raise.
     glance_block_draft_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens) -> (out, lse)
     glance_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents) -> (out, lse)
     glance_greedy_accept(logits, parents, tokens) -> dict(argmax, accept_len, accept_path, next_root)
+    glance_sample_accept(logits, parents, tokens, temperature, seed, round_)
+        -> dict(draws, accept_len, accept_path, next_root)
     glance_build_tree(draft_logits, roots, budget) -> dict(parents, tokens, scores)
     glance_commit_path(k_new, v_new, accept_len, accept_path, k_ctx, v_ctx, ctx_lens)  (in place)
 
@@ -56,6 +58,9 @@ _SIGS = {
                                                _P, _P, _SZ, _P]),
     "glance_greedy_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P, _P, _I32,
                                             _P, _P, _P, _SZ, _P]),
+    "glance_sample_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, ctypes.c_float,
+                                            ctypes.c_uint64, ctypes.c_uint32, _P, _P, _P, _I32, _P, _P, _SZ,
+                                            _P]),
     "glance_build_tree": (ctypes.c_int, [_I32, _I32, _I32, _I32, ctypes.c_int, _P, ctypes.c_int64, _P, _P,
                                          _P, _P, _P, _SZ, _P]),
     "glance_tree_workspace_size": (_SZ, [_I32, _I32, _I32, _I32]),
@@ -291,6 +296,34 @@ def _accept_args(logits, parents, tokens, path_stride, outputs, workspace, strea
             _ptr(outputs.get("root_entropy")), _ptr(ws), ctypes.c_size_t(ws.numel() * ws.element_size()),
             _stream(stream)]
     return args, outputs, ws
+
+
+def glance_sample_accept(logits, parents, tokens, temperature, seed, round_, path_stride=None, outputs=None,
+                         workspace=None, stream=None):
+    """Row draws from softmax(z / temperature) (Gumbel-max over Philox4x32-10
+    noise keyed by seed, counted by round) + the walk of Algorithm 1 over the
+    draws.  Returns a dict of int32 GPU tensors: draws, accept_len,
+    accept_path, next_root."""
+    args, outputs = _sample_args(logits, parents, tokens, temperature, seed, round_, path_stride, outputs,
+                                 workspace, stream)
+    _check(lib().glance_sample_accept(*args))
+    return outputs
+
+
+def _sample_args(logits, parents, tokens, temperature, seed, round_, path_stride, outputs, workspace, stream):
+    torch = _torch()
+    seed, round_ = int(seed), int(round_)
+    if not 0 <= seed < 2 ** 64 or not 0 <= round_ < 2 ** 32:
+        raise ValueError("seed must fit 64 bits and round_ 32 bits, both unsigned")
+    if outputs is not None and "draws" in outputs:
+        outputs = dict(outputs, argmax=outputs["draws"])
+    args, outputs, _ = _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream, False)
+    # glance_greedy_accept's argument list with the row results renamed to draws
+    # and (temperature, seed, round) in place of the root-entropy pointer
+    outputs["draws"] = outputs.pop("argmax")
+    args = args[:7] + [ctypes.c_float(float(temperature)), ctypes.c_uint64(seed), ctypes.c_uint32(round_)] + \
+        args[7:12] + args[13:]
+    return args, outputs
 
 
 def _tree_args(draft_logits, roots, budget, first_row, horizon, outputs, workspace, stream, want_scores):

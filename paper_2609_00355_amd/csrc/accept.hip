@@ -10,6 +10,19 @@
 //                 child that carries the current row's argmax token with one
 //                 ballot per step.
 //
+// sample_partial  the sampling walk's row draws (temperature T > 0): the same
+//                 grid and packed reduction as argmax_partial over
+//                 z / T + g instead of z, with Gumbel noise g = -ln(-ln u);
+//                 accept_walk then walks the draws.  u comes from
+//                 Philox4x32-10 (Salmon et al., SC'11) with key (seed) and
+//                 counter (w / 4, node, sequence, round), word w % 4, mapped
+//                 to ((x >> 9) + 0.5) 2^-23; both logarithms use one fixed
+//                 fp32 recipe (exponent, then 2 atanh(s) with
+//                 s = (m - 1) / (m + 1) as an odd series to s^9) with fused
+//                 multiply-add disabled, so every draw is reproducible bit for
+//                 bit off the GPU.  Tokens that provably cannot win skip the
+//                 logarithms (see sample_partial).
+//
 // Root entropy (optional): the target's next-token entropy at the round root,
 // H = -sum_w p(w) log p(w) over row 0 of each sequence (the scalar of the
 // paper's entropy law, Sec. 4).  The argmax workgroups of row 0 re-read their
@@ -216,6 +229,162 @@ __global__ __launch_bounds__(256) void argmax_partial(AcceptParams p) {
   }
 }
 
+// Philox4x32-10: ten rounds of two 32x32 -> 64-bit multiplies and a
+// counter shuffle, the key advanced by the Weyl constants between rounds.
+__device__ __forceinline__ void philox4x32_10(unsigned (&c)[4], unsigned k0, unsigned k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const unsigned long long p0 = (unsigned long long)0xD2511F53u * c[0];
+    const unsigned long long p1 = (unsigned long long)0xCD9E8D57u * c[2];
+    const unsigned n0 = (unsigned)(p1 >> 32) ^ c[1] ^ k0;
+    const unsigned n2 = (unsigned)(p0 >> 32) ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = (unsigned)p1;
+    c[2] = n2;
+    c[3] = (unsigned)p0;
+  }
+}
+
+// ln t for a positive normal t by the fixed recipe: t = m 2^e with m in
+// [sqrt(1/2), sqrt(2)) (so m - 1 is exact and t near 1 keeps e = 0), then
+// e ln 2 + 2 atanh(s), s = (m - 1) / (m + 1), atanh(s) / s as the series
+// 1 + s^2/3 + ... + s^8/9.  IEEE-rounded operations, no fused multiply-add.
+__device__ __forceinline__ float ln_fixed(float t) {
+#pragma clang fp contract(off)
+  const unsigned bits = __builtin_bit_cast(unsigned, t);
+  const unsigned mant = bits & 0x007FFFFFu;
+  const bool high = mant > 0x3504F3u;  // m >= sqrt(2): halve it
+  const int e = (int)((bits >> 23) & 0xFFu) - 127 + (high ? 1 : 0);
+  const float m = __builtin_bit_cast(float, mant | (high ? 0x3F000000u : 0x3F800000u));
+  const float s = (m - 1.0f) / (m + 1.0f);
+  const float s2 = s * s;
+  float acc = (float)(1.0 / 9.0);
+  acc = acc * s2 + (float)(1.0 / 7.0);
+  acc = acc * s2 + (float)(1.0 / 5.0);
+  acc = acc * s2 + (float)(1.0 / 3.0);
+  acc = acc * s2 + 1.0f;
+  const float at2 = 2.0f * (s * acc);
+  return (float)e * (float)0.6931471805599453 + at2;
+}
+
+// The perturbed logit z / T + g of one token, g = -ln(-ln u), exactly as the
+// definition rounds it.
+__device__ __forceinline__ float gumbel_logit(float z, float temperature, unsigned x) {
+#pragma clang fp contract(off)
+  const float u = ((float)(x >> 9) + 0.5f) * 0x1p-23f;
+  const float g = -ln_fixed(-ln_fixed(u));
+  return z / temperature + g;
+}
+
+// Wave maximum of floats (NaN ignored), broadcast; every lane must be active.
+__device__ __forceinline__ float wave_fmax(float v) {
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0xb1, 0xf, 0xf, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x4e, 0xf, 0xf, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x141, 0xf, 0xf, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x140, 0xf, 0xf, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x142, 0xa, 0xf, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x143, 0xc, 0xf, false)));
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+// Row draws of the sampling walk.  Evaluating both logarithms for every token
+// would make the kernel ALU-bound several times over, so a token is first
+// tested against the wave's running best y* (the largest z / T + g seen by
+// any lane of the wave) with an upper bound on its noise taken from the
+// uniform's integer alone: for u = (k + 0.5) 2^-23 and r = 2^23 - 1 - k,
+// g <= -ln(1 - u) <= (clz(r) - 8) ln 2 (the fixed recipe stays within 1e-7
+// of this bound).  A token is skipped only when z / T plus that bound plus a
+// margin for every rounding involved (2^-17 relative, 2^-12 absolute) is
+// still below y*: then a strictly larger value exists and the token cannot be
+// the draw.  Before the Philox call, the same test with the largest bound,
+// 24 ln 2, skips whole groups of four.  Survivors take the exact definition.
+template <bool BF16>
+__global__ __launch_bounds__(256) void sample_partial(AcceptParams p) {
+  constexpr float kLn2 = 0.6931472f;
+  __shared__ unsigned long long red[4];
+  const int chunk = blockIdx.x % p.chunks;
+  const long row = blockIdx.x / p.chunks;
+  const unsigned node = (unsigned)(row % p.n_nodes), seq = (unsigned)(row / p.n_nodes);
+  const int c0 = chunk * p.chunk_len;  // a multiple of 8: groups of four never straddle chunks
+  const int c1 = min(p.vocab, c0 + p.chunk_len);
+  const int tid = threadIdx.x;
+  const float inv_t = p.inv_temperature;
+  int best_key = (int)0x80000000;
+  int best_idx = 0x7fffffff;
+  float lane_best = -__builtin_inff();  // y of the lane's current best token
+  float wbest = -__builtin_inff();      // maximum of lane_best over the wave
+  for (int base = c0; base < c1; base += 4 * 256) {  // the same trip count for every lane
+    const int e4 = base + 4 * tid;
+    float z[4];
+    if (BF16) {
+      const unsigned short* x = static_cast<const unsigned short*>(p.logits) + row * (long)p.vocab;
+      if (p.sample_vec && e4 + 3 < c1) {
+        const uint2 v = *reinterpret_cast<const uint2*>(x + e4);
+        z[0] = __builtin_bit_cast(float, v.x << 16);
+        z[1] = __builtin_bit_cast(float, v.x & 0xffff0000u);
+        z[2] = __builtin_bit_cast(float, v.y << 16);
+        z[3] = __builtin_bit_cast(float, v.y & 0xffff0000u);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) z[j] = e4 + j < c1 ? __builtin_bit_cast(float, (unsigned)x[e4 + j] << 16) : 0.f;
+      }
+    } else {
+      const float* x = static_cast<const float*>(p.logits) + row * (long)p.vocab;
+      if (p.sample_vec && e4 + 3 < c1) {
+        const float4 v = *reinterpret_cast<const float4*>(x + e4);
+        z[0] = v.x;
+        z[1] = v.y;
+        z[2] = v.z;
+        z[3] = v.w;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) z[j] = e4 + j < c1 ? x[e4 + j] : 0.f;
+      }
+    }
+    const float slack = fmaf(fabsf(wbest), 0x1p-17f, 0x1p-12f);
+    float lo[4];  // z / T raised by its rounding allowance and the slack
+    bool cand[4];
+    bool any = false;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float zt = z[j] * inv_t;
+      lo[j] = fmaf(fabsf(zt), 0x1p-17f, zt) + slack;
+      const bool beaten = (z[j] == -__builtin_inff()) ? (wbest > -__builtin_inff()) : (lo[j] + 24.f * kLn2 < wbest);
+      cand[j] = e4 + j < c1 && !beaten;
+      any |= cand[j];
+    }
+    if (any) {
+      unsigned c[4] = {(unsigned)e4 >> 2, node, seq, p.round};
+      philox4x32_10(c, p.seed_lo, p.seed_hi);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const unsigned r = 0x7FFFFFu - (c[j] >> 9);
+        const int lz = r ? __builtin_clz(r) : 32;
+        const bool beaten = (z[j] != -__builtin_inff()) && (lo[j] + (float)(lz - 8) * kLn2 < wbest);
+        if (cand[j] && !beaten) {
+          const float y = gumbel_logit(z[j], p.temperature, c[j]);
+          const int k = order_key(__builtin_bit_cast(unsigned, y));
+          if (k > best_key) {
+            best_key = k;
+            best_idx = e4 + j;
+            lane_best = y;
+          }
+        }
+      }
+    }
+    wbest = fmaxf(wbest, wave_fmax(lane_best));
+  }
+  unsigned long long w = (best_idx == 0x7fffffff) ? 0ull : pack(best_key, best_idx);
+  w = wave_max64(w);
+  if ((tid & 63) == 0) red[tid >> 6] = w;
+  __syncthreads();
+  if (tid == 0) p.part[row * p.chunks + chunk] = umax64(umax64(red[0], red[1]), umax64(red[2], red[3]));
+}
+
 __global__ __launch_bounds__(64) void accept_walk(AcceptParams p) {
   __shared__ int sAm[64];
   const int b = blockIdx.x;
@@ -277,6 +446,24 @@ __global__ __launch_bounds__(64) void accept_walk(AcceptParams p) {
 }
 
 }  // namespace
+
+hipError_t launch_sample(const AcceptParams& p_in, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  AcceptParams p = p_in;
+  const long rows = (long)p.batch * p.n_nodes;
+  const dim3 grid((unsigned)(rows * p.chunks)), block(256);
+  const size_t vbytes = bf16 ? 8 : 16;  // one group of four tokens
+  p.sample_vec = ((size_t)p.vocab * (bf16 ? 2 : 4)) % vbytes == 0 &&
+                 (reinterpret_cast<uintptr_t>(p.logits) % vbytes) == 0;
+  p.root_entropy = nullptr;
+  if (ev0) (void)hipEventRecord(ev0, s);
+  if (bf16) hipLaunchKernelGGL(sample_partial<true>, grid, block, 0, s, p);
+  else hipLaunchKernelGGL(sample_partial<false>, grid, block, 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (ev1) (void)hipEventRecord(ev1, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(accept_walk, dim3(p.batch), dim3(64), 0, s, p);
+  return hipGetLastError();
+}
 
 hipError_t launch_accept(const AcceptParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const long rows = (long)p.batch * p.n_nodes;

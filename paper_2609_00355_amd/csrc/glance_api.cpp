@@ -10,6 +10,8 @@
 
 #include <string>
 
+#include <cfloat>
+
 #include "glance_internal.h"
 
 namespace {
@@ -371,6 +373,66 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
   take_events(&e0, &e1);
   return check_hip(glance::launch_accept(p, logits_dtype == GLANCE_BF16, stream, e0, e1),
                    "accept kernel launch");
+}
+
+glance_status glance_sample_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                   glance_dtype logits_dtype, const void* logits,
+                                   const int32_t* parents, const int32_t* tokens, float temperature,
+                                   uint64_t seed, uint32_t round, int32_t* draws_out,
+                                   int32_t* accept_len, int32_t* accept_path, int32_t path_stride,
+                                   int32_t* next_root, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  AcceptPlan pl;
+  glance_status st = accept_plan(batch, n_nodes, vocab, &pl);
+  if (st != GLANCE_OK) return st;
+  if (logits_dtype != GLANCE_F32 && logits_dtype != GLANCE_BF16)
+    return fail(GLANCE_ERR_UNSUPPORTED, "logits dtype must be GLANCE_F32 or GLANCE_BF16");
+  if (!(temperature >= FLT_MIN) || !(temperature <= FLT_MAX))
+    return fail(GLANCE_ERR_INVALID_ARG, "temperature must be a finite normal float > 0 (got %g)",
+                (double)temperature);
+  if (path_stride < 1) return fail(GLANCE_ERR_INVALID_ARG, "path_stride must be >= 1");
+  struct {
+    const void* ptr;
+    const char* name;
+  } req[] = {{logits, "logits"},       {parents, "parents"},         {tokens, "tokens"},
+             {draws_out, "draws_out"}, {accept_len, "accept_len"}, {accept_path, "accept_path"},
+             {next_root, "next_root"}};
+  for (auto& r : req) {
+    if (!r.ptr) return fail(GLANCE_ERR_INVALID_ARG, "%s is NULL", r.name);
+    if (reinterpret_cast<uintptr_t>(r.ptr) & 3u) return fail(GLANCE_ERR_INVALID_ARG, "%s is not 4-byte aligned", r.name);
+  }
+  if (logits_dtype == GLANCE_BF16 && (reinterpret_cast<uintptr_t>(logits) & 1u))
+    return fail(GLANCE_ERR_INVALID_ARG, "logits is not 2-byte aligned");
+  if (!workspace) return fail(GLANCE_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(GLANCE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < pl.bytes)
+    return fail(GLANCE_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes,
+                pl.bytes);
+  glance::AcceptParams p = {};
+  p.logits = logits;
+  p.parents = parents;
+  p.tokens = tokens;
+  p.argmax_out = draws_out;
+  p.accept_len = accept_len;
+  p.accept_path = accept_path;
+  p.next_root = next_root;
+  p.part = static_cast<unsigned long long*>(workspace);
+  p.batch = batch;
+  p.n_nodes = n_nodes;
+  p.vocab = vocab;
+  p.path_stride = path_stride;
+  p.chunks = pl.chunks;
+  p.chunk_len = pl.chunk_len;
+  p.temperature = temperature;
+  p.inv_temperature = 1.0f / temperature;
+  p.seed_lo = (unsigned)(seed & 0xffffffffu);
+  p.seed_hi = (unsigned)(seed >> 32);
+  p.round = round;
+  hipEvent_t e0, e1;
+  take_events(&e0, &e1);
+  return check_hip(glance::launch_sample(p, logits_dtype == GLANCE_BF16, stream, e0, e1),
+                   "sample kernel launch");
 }
 
 glance_status glance_build_tree(int32_t batch, int32_t horizon, int32_t vocab, int32_t budget,

@@ -62,6 +62,10 @@ struct AcceptParams {
   float4* ent_part;          // [batch][chunks] (chunk max m, sum e^(z-m), sum e^(z-m) (z-m), 0)
   int batch, n_nodes, vocab, path_stride;
   int chunks, chunk_len;     // chunk_len is a multiple of 8
+  // sampling walk only: the row draws are argmax(z / temperature + Gumbel)
+  float temperature, inv_temperature;
+  unsigned seed_lo, seed_hi, round;
+  int sample_vec;            // rows allow aligned loads of four tokens
 };
 
 // Draft tree builder.  Limits: budget N <= kTreeMaxBudget strings below the
@@ -123,6 +127,7 @@ hipError_t launch_attn_bf16(const AttnParams& p, bool tree, hipStream_t s, hipEv
 hipError_t launch_attn_f32(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_attn_merge(const AttnParams& p, bool out_bf16, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+hipError_t launch_sample(const AcceptParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_tree(const TreeParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_commit(const CommitParams& p, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 

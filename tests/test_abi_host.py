@@ -128,6 +128,23 @@ def test_accept_argument_checks(lib):
     assert st == G.GLANCE_ERR_WORKSPACE
 
 
+def _sample(lib, n=8, temperature=1.0, parents=FAKE, draws=FAKE, ws=FAKE, ws_bytes=1 << 20, dtype=G.GLANCE_BF16):
+    return lib.glance_sample_accept(1, n, 100, dtype, FAKE, parents, FAKE, temperature, 2 ** 64 - 1, 2 ** 32 - 1,
+                                    draws, FAKE, FAKE, 8, FAKE, ws, ws_bytes, None)
+
+
+def test_sample_argument_checks(lib):
+    for t in (0.0, -1.0, float("inf"), float("nan"), 1e-39):
+        assert _sample(lib, temperature=t) == G.GLANCE_ERR_INVALID_ARG
+        assert "temperature" in G.glance_last_error()
+    assert _sample(lib, n=65) == G.GLANCE_ERR_UNSUPPORTED
+    assert _sample(lib, parents=None) == G.GLANCE_ERR_INVALID_ARG and "parents" in G.glance_last_error()
+    assert _sample(lib, draws=None) == G.GLANCE_ERR_INVALID_ARG and "draws_out" in G.glance_last_error()
+    assert _sample(lib, ws_bytes=1) == G.GLANCE_ERR_WORKSPACE
+    assert _sample(lib, ws=ctypes.c_void_p(0x10010)) == G.GLANCE_ERR_WORKSPACE
+    assert _sample(lib, dtype=7) == G.GLANCE_ERR_UNSUPPORTED
+
+
 def _build_tree(lib, batch=1, horizon=15, vocab=152064, budget=63, dtype=G.GLANCE_BF16, logits=FAKE,
                 stride=None, roots=FAKE, parents=FAKE, tokens=FAKE, scores=FAKE, ws=FAKE, ws_bytes=1 << 30):
     stride = horizon * vocab if stride is None else stride
