@@ -31,6 +31,15 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
+# Vector ALU issue peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12
+# full-rate lane operations per second (a 32x32 -> 64-bit multiply issues at
+# a quarter of that rate and counts as 4).
+VALU_PEAK_TOPS = 39.32
+# Work of the sampling walk's row draws per token, in full-rate lane
+# operations: a quarter of one Philox4x32-10 call (20 64-bit multiplies at 4
+# each plus 20 three-input XORs: 100 per four tokens = 25), the noise bound and
+# its test (8), and the load and unpack of a bf16 pair (1).
+SAMPLE_OPS_PER_TOKEN = 34
 
 
 def parse():
@@ -100,9 +109,11 @@ COPY_BYTES = 256 << 20
 COPY_KERNEL = "neg_kernel"  # the calibration copy: out = -in over COPY_BYTES of fp32
 KERNEL_KEYS = {"draft": "attn_bf16_partial<128, false", "verify": "attn_bf16_partial<128, true",
                "accept": "argmax_partial<true, true>", "tree_stats": "tree_stats<true>",
-               "tree_cands": "tree_cands<true>", "tree_rank": "tree_rank<true>", "tree_enum": "tree_enum"}
+               "tree_cands": "tree_cands<true>", "tree_rank": "tree_rank<true>", "tree_enum": "tree_enum",
+               "sample": "sample_partial<true, true>"}
 KERNEL_SRC = {"draft": "attn_bf16.hip", "verify": "attn_bf16.hip", "accept": "accept.hip",
-              "tree_stats": "tree.hip", "tree_cands": "tree.hip", "tree_rank": "tree.hip", "tree_enum": "tree.hip"}
+              "tree_stats": "tree.hip", "tree_cands": "tree.hip", "tree_rank": "tree.hip", "tree_enum": "tree.hip",
+              "sample": "accept.hip"}
 
 
 def summarise_traffic(fetch_dir, write_dir):
@@ -296,6 +307,44 @@ def measure_commit(args, w, s, G, torch, np, dev, stream, ctx):
             "bound": "launch latency (a few KB per call)"}
 
 
+def measure_sample(args, w, sets, G, torch, np, stream):
+    """The sampling walk at temperature 1 (glance_sample_accept) on the round's
+    verified logits, in place of the greedy acceptance: HIP events around its
+    row-draw kernel, mean over the steps, the round number advancing every call
+    so every call draws fresh noise."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, b in evs:
+        a.record(stream)
+        b.record(stream)
+    outs = []
+    for s in sets:
+        logits, par, tok = s["keep"][4], s["keep"][2], s["keep"][3]
+        outs.append(G.glance_sample_accept(logits, par, tok, 1.0, 2026, 0, path_stride=16, stream=stream))
+    torch.cuda.synchronize()
+    for i in range(args.warmup + args.steps):
+        s = sets[i % len(sets)]
+        logits, par, tok = s["keep"][4], s["keep"][2], s["keep"][3]
+        if i >= args.warmup:
+            G.glance_set_kernel_events(*evs[i - args.warmup])
+        G.glance_sample_accept(logits, par, tok, 1.0, 2026, i + 1, path_stride=16,
+                               outputs=outs[i % len(sets)], stream=stream)
+    torch.cuda.synchronize()
+    us = float(np.mean([a.elapsed_time(b) for a, b in evs]) * 1e3)
+    tokens = w.batch * w.n_tree * w.vocab
+    nbytes = tokens * 2
+    acc = outs[0]["accept_len"].cpu().numpy()
+    ops = tokens * SAMPLE_OPS_PER_TOKEN
+    return {"us": round(us, 2), "kernel": "sample_partial<true,true>",
+            "input": f"verified logits {w.batch} x {w.n_tree} x {w.vocab} bf16, T = 1",
+            "gtokens_per_s": round(tokens / us / 1e3, 1), "gbps": round(nbytes / us / 1e3, 1),
+            "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4), "bound": "alu",
+            "alu_ops_per_token": SAMPLE_OPS_PER_TOKEN, "achieved_tops": round(ops / us / 1e6, 2),
+            "peak_tops": VALU_PEAK_TOPS, "frac": round(ops / us / 1e6 / VALU_PEAK_TOPS, 4),
+            "traffic": load_traffic("sample", os.path.join(ROOT, "paper_2609_00355_amd", "csrc", "accept.hip")),
+            "mean_accept_len": round(float(acc.mean()), 3)}
+
+
 def main():
     args = parse()
     if args.traffic_from:
@@ -457,6 +506,7 @@ def main():
 
     tree = None if args.no_tree else measure_tree_builder(args, w, G, C, torch, np, dev, stream)
     commit = measure_commit(args, w, sets[0], G, torch, np, dev, stream, ctx)
+    sample = measure_sample(args, w, sets, G, torch, np, stream)
 
     acc = sets[0]["a_out"]["accept_len"].cpu().numpy()
     res = {
@@ -489,6 +539,7 @@ def main():
     if tree is not None:
         res["tree_builder"] = tree
     res["commit"] = commit
+    res["sample_accept"] = sample
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(inputs, args.cpu_seconds)
     print(json.dumps(res), flush=True)

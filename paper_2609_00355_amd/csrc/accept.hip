@@ -240,8 +240,9 @@ __device__ __forceinline__ void philox4x32_10(unsigned (&c)[4], unsigned k0, uns
     }
     const unsigned long long p0 = (unsigned long long)0xD2511F53u * c[0];
     const unsigned long long p1 = (unsigned long long)0xCD9E8D57u * c[2];
-    const unsigned n0 = (unsigned)(p1 >> 32) ^ c[1] ^ k0;
-    const unsigned n2 = (unsigned)(p0 >> 32) ^ c[3] ^ k1;
+    // three-input XOR in one v_bitop3_b32 (truth table 0x96)
+    const unsigned n0 = __builtin_amdgcn_bitop3_b32((unsigned)(p1 >> 32), c[1], k0, 0x96);
+    const unsigned n2 = __builtin_amdgcn_bitop3_b32((unsigned)(p0 >> 32), c[3], k1, 0x96);
     c[0] = n0;
     c[1] = (unsigned)p1;
     c[2] = n2;
@@ -280,105 +281,157 @@ __device__ __forceinline__ float gumbel_logit(float z, float temperature, unsign
   return z / temperature + g;
 }
 
-// Wave maximum of floats (NaN ignored), broadcast; every lane must be active.
-__device__ __forceinline__ float wave_fmax(float v) {
-  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0xb1, 0xf, 0xf, false)));
-  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x4e, 0xf, 0xf, false)));
-  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x141, 0xf, 0xf, false)));
-  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x140, 0xf, 0xf, false)));
-  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x142, 0xa, 0xf, false)));
-  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v), 0x143, 0xc, 0xf, false)));
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+// Monotone map between floats and signed integers (its own inverse): larger
+// numbers give larger keys; a positive NaN maps above +inf.
+__device__ __forceinline__ int float_order(int bits) { return bits ^ ((bits >> 31) & 0x7fffffff); }
+
+// Wave maximum of integer keys, broadcast; every lane must be active.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dpp_i(int v) {  // lanes a row mask leaves out read INT_MIN
+  return __builtin_amdgcn_update_dpp((int)0x80000000, v, CTRL, ROWS, 0xf, false);
+}
+__device__ __forceinline__ int wave_max_key(int v) {
+  v = max(v, dpp_i<0xb1, 0xf>(v));
+  v = max(v, dpp_i<0x4e, 0xf>(v));
+  v = max(v, dpp_i<0x141, 0xf>(v));
+  v = max(v, dpp_i<0x140, 0xf>(v));
+  v = max(v, dpp_i<0x142, 0xa>(v));
+  v = max(v, dpp_i<0x143, 0xc>(v));
+  return __builtin_amdgcn_readlane(v, 63);
+}
+
+// One group of four tokens as raw words (bf16 pairs, or fp32 bits), loaded a
+// loop iteration ahead and unpacked when used.
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void load_group(const void* rowp, int e4, unsigned (&w)[4]) {
+  if (BF16) {
+    const unsigned short* x = static_cast<const unsigned short*>(rowp);
+    if (VEC) {
+      const uint2 v = *reinterpret_cast<const uint2*>(x + e4);
+      w[0] = v.x;
+      w[1] = v.y;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[j] = x[e4 + j];
+    }
+  } else {
+    const unsigned* x = static_cast<const unsigned*>(rowp);
+    if (VEC) {
+      const uint4 v = *reinterpret_cast<const uint4*>(x + e4);
+      w[0] = v.x;
+      w[1] = v.y;
+      w[2] = v.z;
+      w[3] = v.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[j] = x[e4 + j];
+    }
+  }
+}
+
+template <bool BF16, bool VEC>
+__device__ __forceinline__ void unpack_group(const unsigned (&w)[4], float (&z)[4]) {
+  if (BF16 && VEC) {
+    z[0] = __builtin_bit_cast(float, w[0] << 16);
+    z[1] = __builtin_bit_cast(float, w[0] & 0xffff0000u);
+    z[2] = __builtin_bit_cast(float, w[1] << 16);
+    z[3] = __builtin_bit_cast(float, w[1] & 0xffff0000u);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) z[j] = __builtin_bit_cast(float, BF16 ? w[j] << 16 : w[j]);
+  }
 }
 
 // Row draws of the sampling walk.  Evaluating both logarithms for every token
-// would make the kernel ALU-bound several times over, so a token is first
-// tested against the wave's running best y* (the largest z / T + g seen by
-// any lane of the wave) with an upper bound on its noise taken from the
-// uniform's integer alone: for u = (k + 0.5) 2^-23 and r = 2^23 - 1 - k,
-// g <= -ln(1 - u) <= (clz(r) - 8) ln 2 (the fixed recipe stays within 1e-7
-// of this bound).  A token is skipped only when z / T plus that bound plus a
-// margin for every rounding involved (2^-17 relative, 2^-12 absolute) is
-// still below y*: then a strictly larger value exists and the token cannot be
-// the draw.  Before the Philox call, the same test with the largest bound,
-// 24 ln 2, skips whole groups of four.  Survivors take the exact definition.
-template <bool BF16>
-__global__ __launch_bounds__(256) void sample_partial(AcceptParams p) {
+// would cost about a hundred instructions a token, so each token is first
+// tested against the wave's running best y* (the largest z / T + g found so
+// far by any lane of the wave) with an upper bound on its noise read off the
+// uniform's integer: with u = (k + 0.5) 2^-23, r = 2^23 - 1 - k and x the
+// generator word (k = x >> 9), g <= -ln(1 - u) <= (clz(r) - 8) ln 2, and
+// clz(r) - 8 = min(L, 23) + 1 when u >= 1/2, L being the leading one bits of
+// x (v_ffbh_i32); for u < 1/2 the same expression is >= ln 2 > g(1/2).  The
+// fixed recipe stays within 1e-7 of this bound.  A token is skipped only when
+// z / T plus that bound plus a margin for every rounding involved (2^-17
+// relative, 2^-12 absolute) is still below y*: then a strictly larger value
+// exists and the token cannot be the draw.  Before the generator runs, the
+// largest bound, 24 ln 2, tests the group's largest logit (NaN-propagating)
+// to skip whole groups of four.  -inf logits are clamped to -FLT_MAX for the
+// group test, so fully masked groups are skipped once y* is finite.  Survivors take the
+// exact definition.  (A -inf logit inside a group with finite ones gives a NaN
+// bound and takes the exact path: slower, never wrong.)
+struct SampleState {
+  int best_key, best_idx;
+  float lane_best;  // y of the lane's best token
+};
+
+template <bool TAIL>
+__device__ __forceinline__ void sample_group(const AcceptParams& p, const float (&z)[4], int e4, int c1,
+                                             unsigned node, unsigned seq, float wbest, SampleState& st) {
   constexpr float kLn2 = 0.6931472f;
+  const float inv_t = p.inv_temperature;
+  const float slack = fmaf(fabsf(wbest), 0x1p-17f, 0x1p-12f);
+  // group test with the largest bound
+  float m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(z[0], z[1]),
+                                          __builtin_elementwise_maximum(z[2], z[3]));
+  float mt = m * inv_t;
+  mt = mt == -__builtin_inff() ? -3.4028234663852886e38f : mt;
+  const bool group_beaten = fmaf(fabsf(mt), 0x1p-17f, mt) + (slack + 24.f * kLn2) < wbest;
+  if (group_beaten && !TAIL) return;
+  if (TAIL && (group_beaten || e4 >= c1)) return;
+  unsigned c[4] = {(unsigned)e4 >> 2, node, seq, p.round};
+  philox4x32_10(c, p.seed_lo, p.seed_hi);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (TAIL && e4 + j >= c1) break;
+    const float zt = z[j] * inv_t;
+    const int lead = min(__builtin_clrsb((int)c[j]) + 1, 23);  // leading bits equal to the top bit
+    const float bound = fmaf((float)lead, kLn2, fmaf(fabsf(zt), 0x1p-17f, zt) + (slack + kLn2));
+    if (!(bound < wbest)) {
+      const float y = gumbel_logit(z[j], p.temperature, c[j]);
+      const int k = order_key(__builtin_bit_cast(unsigned, y));
+      if (k > st.best_key) {
+        st.best_key = k;
+        st.best_idx = e4 + j;
+        st.lane_best = y;
+      }
+    }
+  }
+}
+
+template <bool BF16, bool VEC>
+__global__ __launch_bounds__(256) void sample_partial(AcceptParams p) {
   __shared__ unsigned long long red[4];
   const int chunk = blockIdx.x % p.chunks;
   const long row = blockIdx.x / p.chunks;
   const unsigned node = (unsigned)(row % p.n_nodes), seq = (unsigned)(row / p.n_nodes);
   const int c0 = chunk * p.chunk_len;  // a multiple of 8: groups of four never straddle chunks
   const int c1 = min(p.vocab, c0 + p.chunk_len);
+  const int full_end = c0 + (c1 - c0) / 1024 * 1024;  // iterations where every lane has four tokens
   const int tid = threadIdx.x;
-  const float inv_t = p.inv_temperature;
-  int best_key = (int)0x80000000;
-  int best_idx = 0x7fffffff;
-  float lane_best = -__builtin_inff();  // y of the lane's current best token
-  float wbest = -__builtin_inff();      // maximum of lane_best over the wave
-  for (int base = c0; base < c1; base += 4 * 256) {  // the same trip count for every lane
-    const int e4 = base + 4 * tid;
+  const char* rowp = static_cast<const char*>(p.logits) + row * (long)p.vocab * (BF16 ? 2 : 4);
+  SampleState st = {(int)0x80000000, 0x7fffffff, -__builtin_inff()};
+  float wbest = -__builtin_inff();  // maximum of lane_best over the wave
+  unsigned wn[4] = {0u, 0u, 0u, 0u};
+  if (c0 < full_end) load_group<BF16, VEC>(rowp, c0 + 4 * tid, wn);
+  for (int base = c0; base < full_end; base += 1024) {  // the same trip count for every lane
     float z[4];
-    if (BF16) {
-      const unsigned short* x = static_cast<const unsigned short*>(p.logits) + row * (long)p.vocab;
-      if (p.sample_vec && e4 + 3 < c1) {
-        const uint2 v = *reinterpret_cast<const uint2*>(x + e4);
-        z[0] = __builtin_bit_cast(float, v.x << 16);
-        z[1] = __builtin_bit_cast(float, v.x & 0xffff0000u);
-        z[2] = __builtin_bit_cast(float, v.y << 16);
-        z[3] = __builtin_bit_cast(float, v.y & 0xffff0000u);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) z[j] = e4 + j < c1 ? __builtin_bit_cast(float, (unsigned)x[e4 + j] << 16) : 0.f;
-      }
-    } else {
-      const float* x = static_cast<const float*>(p.logits) + row * (long)p.vocab;
-      if (p.sample_vec && e4 + 3 < c1) {
-        const float4 v = *reinterpret_cast<const float4*>(x + e4);
-        z[0] = v.x;
-        z[1] = v.y;
-        z[2] = v.z;
-        z[3] = v.w;
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) z[j] = e4 + j < c1 ? x[e4 + j] : 0.f;
-      }
-    }
-    const float slack = fmaf(fabsf(wbest), 0x1p-17f, 0x1p-12f);
-    float lo[4];  // z / T raised by its rounding allowance and the slack
-    bool cand[4];
-    bool any = false;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float zt = z[j] * inv_t;
-      lo[j] = fmaf(fabsf(zt), 0x1p-17f, zt) + slack;
-      const bool beaten = (z[j] == -__builtin_inff()) ? (wbest > -__builtin_inff()) : (lo[j] + 24.f * kLn2 < wbest);
-      cand[j] = e4 + j < c1 && !beaten;
-      any |= cand[j];
-    }
-    if (any) {
-      unsigned c[4] = {(unsigned)e4 >> 2, node, seq, p.round};
-      philox4x32_10(c, p.seed_lo, p.seed_hi);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const unsigned r = 0x7FFFFFu - (c[j] >> 9);
-        const int lz = r ? __builtin_clz(r) : 32;
-        const bool beaten = (z[j] != -__builtin_inff()) && (lo[j] + (float)(lz - 8) * kLn2 < wbest);
-        if (cand[j] && !beaten) {
-          const float y = gumbel_logit(z[j], p.temperature, c[j]);
-          const int k = order_key(__builtin_bit_cast(unsigned, y));
-          if (k > best_key) {
-            best_key = k;
-            best_idx = e4 + j;
-            lane_best = y;
-          }
-        }
-      }
-    }
-    wbest = fmaxf(wbest, wave_fmax(lane_best));
+    unpack_group<BF16, VEC>(wn, z);
+    if (base + 1024 < full_end) load_group<BF16, VEC>(rowp, base + 1024 + 4 * tid, wn);
+    sample_group<false>(p, z, base + 4 * tid, c1, node, seq, wbest, st);
+    const float wm = __builtin_bit_cast(float, float_order(wave_max_key(float_order(__builtin_bit_cast(int, st.lane_best)))));
+    wbest = wm > wbest ? wm : wbest;  // a NaN maximum leaves wbest as it is
   }
-  unsigned long long w = (best_idx == 0x7fffffff) ? 0ull : pack(best_key, best_idx);
+  if (full_end < c1) {  // the ragged tail: per-token bounds checks
+    const int e4 = full_end + 4 * tid;
+    float z[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      z[j] = e4 + j < c1 ? (BF16 ? __builtin_bit_cast(float, (unsigned)reinterpret_cast<const unsigned short*>(rowp)[e4 + j] << 16)
+                                 : reinterpret_cast<const float*>(rowp)[e4 + j])
+                         : -__builtin_inff();
+    sample_group<true>(p, z, e4, c1, node, seq, wbest, st);
+  }
+  unsigned long long w = (st.best_idx == 0x7fffffff) ? 0ull : pack(st.best_key, st.best_idx);
   w = wave_max64(w);
   if ((tid & 63) == 0) red[tid >> 6] = w;
   __syncthreads();
@@ -447,21 +500,26 @@ __global__ __launch_bounds__(64) void accept_walk(AcceptParams p) {
 
 }  // namespace
 
-hipError_t launch_sample(const AcceptParams& p_in, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  AcceptParams p = p_in;
+hipError_t launch_sample(const AcceptParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const long rows = (long)p.batch * p.n_nodes;
   const dim3 grid((unsigned)(rows * p.chunks)), block(256);
   const size_t vbytes = bf16 ? 8 : 16;  // one group of four tokens
-  p.sample_vec = ((size_t)p.vocab * (bf16 ? 2 : 4)) % vbytes == 0 &&
-                 (reinterpret_cast<uintptr_t>(p.logits) % vbytes) == 0;
-  p.root_entropy = nullptr;
+  const bool vec = ((size_t)p.vocab * (bf16 ? 2 : 4)) % vbytes == 0 &&
+                   (reinterpret_cast<uintptr_t>(p.logits) % vbytes) == 0;
   if (ev0) (void)hipEventRecord(ev0, s);
-  if (bf16) hipLaunchKernelGGL(sample_partial<true>, grid, block, 0, s, p);
-  else hipLaunchKernelGGL(sample_partial<false>, grid, block, 0, s, p);
+  if (bf16) {
+    if (vec) hipLaunchKernelGGL((sample_partial<true, true>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((sample_partial<true, false>), grid, block, 0, s, p);
+  } else {
+    if (vec) hipLaunchKernelGGL((sample_partial<false, true>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((sample_partial<false, false>), grid, block, 0, s, p);
+  }
   hipError_t e = hipGetLastError();
   if (ev1) (void)hipEventRecord(ev1, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_walk, dim3(p.batch), dim3(64), 0, s, p);
+  AcceptParams pw = p;
+  pw.root_entropy = nullptr;
+  hipLaunchKernelGGL(accept_walk, dim3(p.batch), dim3(64), 0, s, pw);
   return hipGetLastError();
 }
 

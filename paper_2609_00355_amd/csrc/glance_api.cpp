@@ -200,7 +200,8 @@ glance_status attn_common(bool tree, const glance_attn_shape* s, const void* q, 
 }
 
 struct AcceptPlan {
-  int chunks, chunk_len;
+  int chunks, chunk_len;                // greedy acceptance (bandwidth-bound)
+  int sample_chunks, sample_chunk_len;  // sampling walk (ALU-bound: more workgroups)
   size_t part_bytes, bytes;
 };
 
@@ -226,7 +227,25 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
   chunks = ((long long)vocab + len - 1) / len;
   out->chunks = (int)chunks;
   out->chunk_len = (int)len;
-  out->part_bytes = round_up((size_t)rows * chunks * sizeof(unsigned long long), 256);
+  // sampling: about 1024 workgroups (four waves a SIMD; measured best of
+  // 512..4096 at 256 x 152064 bf16), chunks a multiple of 1024 tokens so that
+  // only a row's last chunk has a ragged tail
+  long long s_target = 1024;
+  if (const char* e = getenv("GLANCE_SAMPLE_WGS")) {  // tuning override
+    const long long v = atoll(e);
+    if (v >= 1 && v <= (1 << 20)) s_target = v;
+  }
+  long long s_chunks = (s_target + rows - 1) / rows;
+  const long long s_max = ((long long)vocab + 4095) / 4096;
+  if (s_chunks > s_max) s_chunks = s_max;
+  if (s_chunks < 1) s_chunks = 1;
+  long long s_len = ((long long)vocab + s_chunks - 1) / s_chunks;
+  s_len = (s_len + 1023) / 1024 * 1024;
+  s_chunks = ((long long)vocab + s_len - 1) / s_len;
+  out->sample_chunks = (int)s_chunks;
+  out->sample_chunk_len = (int)s_len;
+  const long long max_chunks_any = chunks > s_chunks ? chunks : s_chunks;
+  out->part_bytes = round_up((size_t)rows * max_chunks_any * sizeof(unsigned long long), 256);
   out->bytes = out->part_bytes + round_up((size_t)batch * chunks * sizeof(float4), 256);
   return ok();
 }
@@ -422,8 +441,8 @@ glance_status glance_sample_accept(int32_t batch, int32_t n_nodes, int32_t vocab
   p.n_nodes = n_nodes;
   p.vocab = vocab;
   p.path_stride = path_stride;
-  p.chunks = pl.chunks;
-  p.chunk_len = pl.chunk_len;
+  p.chunks = pl.sample_chunks;
+  p.chunk_len = pl.sample_chunk_len;
   p.temperature = temperature;
   p.inv_temperature = 1.0f / temperature;
   p.seed_lo = (unsigned)(seed & 0xffffffffu);

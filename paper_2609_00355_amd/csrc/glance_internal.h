@@ -65,7 +65,6 @@ struct AcceptParams {
   // sampling walk only: the row draws are argmax(z / temperature + Gumbel)
   float temperature, inv_temperature;
   unsigned seed_lo, seed_hi, round;
-  int sample_vec;            // rows allow aligned loads of four tokens
 };
 
 // Draft tree builder.  Limits: budget N <= kTreeMaxBudget strings below the

@@ -154,15 +154,25 @@ def test_sampling_walk_preserves_the_target_distribution():
 
 def test_gumbel_bound_by_leading_zeros():
     """g(u) <= -ln(1 - u) <= (clz(r) - 8) ln 2 with r = 2^23 - 1 - k for the
-    uniform u = (k + 0.5) 2^-23 (since -ln u >= 1 - u and 1 - u >= r 2^-23):
-    an upper bound on the noise from the integer alone, which lets a sampler
-    skip the logarithms of tokens that cannot win.  Checked for every k on the
-    fixed recipe's values, with 2^-16 to spare for its rounding."""
+    uniform u = (k + 0.5) 2^-23 (since -ln u >= 1 - u and 1 - u >= r 2^-23).
+    For u >= 1/2, clz(r) - 8 = min(L, 23) + 1 with L the leading one bits of
+    k; for u < 1/2 the same expression with L the leading zero bits is >= ln 2,
+    above g(1/2) = -ln ln 2.  So (min(L, 23) + 1) ln 2, L the leading bits
+    equal to the top bit, bounds the noise from the integer alone, which lets
+    a sampler skip the logarithms of tokens that cannot win.  Checked for
+    every k on the fixed recipe's values, with 2^-16 to spare for its rounding."""
     k = np.arange(2 ** 23, dtype=np.uint32)
     u = (k.astype(np.float32) + np.float32(0.5)) * np.float32(2.0 ** -23)
     g = S.gumbel(u).astype(np.float64)
+    top = (k >> np.uint32(22)) & np.uint32(1)
+    flipped = np.where(top == 1, np.uint32(0x7FFFFF) - k, k).astype(np.int64)   # leading equal bits -> zeros
+    lead = np.full(k.shape, 23, dtype=np.int64)
+    nz = flipped > 0
+    lead[nz] = 22 - np.floor(np.log2(flipped[nz].astype(np.float64))).astype(np.int64)
+    bound = (np.minimum(lead, 23) + 1) * np.log(2.0)
+    assert np.all(g <= bound + 2.0 ** -16)
+    # the same bound read as clz(r) - 8 for u >= 1/2
     r = (np.uint32(0x7FFFFF) - k).astype(np.int64)
-    clz = np.full(r.shape, 32, dtype=np.int64)
-    nz = r > 0
-    clz[nz] = 31 - np.floor(np.log2(r[nz].astype(np.float64))).astype(np.int64)
-    assert np.all(g <= (clz - 8) * np.log(2.0) + 2.0 ** -16)
+    hi = top == 1
+    clz = np.where(r > 0, 31 - np.floor(np.log2(np.maximum(r, 1).astype(np.float64))).astype(np.int64), 32)
+    assert np.array_equal((clz - 8)[hi], (np.minimum(lead, 23) + 1)[hi])
