@@ -364,28 +364,51 @@ struct SampleState {
   float lane_best;  // y of the lane's best token
 };
 
-template <bool TAIL>
+// One group of four tokens of one lane.  FIRST (the wave's first full
+// group, no running best yet): the wave first takes the largest lower bound
+// on z / T + g over its 256 tokens as y*, from the integer alone:
+// g >= (min(L, 23) - 1) ln 2 for u >= 1/2 (since -ln u <= 2 (1 - u) there)
+// and g >= -2.82 for u < 1/2, less the same rounding allowance; every value
+// is at most some token's exact z / T + g, and the token reaching it is never
+// skipped, so the exact draw is kept.
+template <bool TAIL, bool FIRST>
 __device__ __forceinline__ void sample_group(const AcceptParams& p, const float (&z)[4], int e4, int c1,
-                                             unsigned node, unsigned seq, float wbest, SampleState& st) {
+                                             unsigned node, unsigned seq, float& wbest, SampleState& st) {
   constexpr float kLn2 = 0.6931472f;
   const float inv_t = p.inv_temperature;
-  const float slack = fmaf(fabsf(wbest), 0x1p-17f, 0x1p-12f);
-  // group test with the largest bound
-  float m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(z[0], z[1]),
-                                          __builtin_elementwise_maximum(z[2], z[3]));
-  float mt = m * inv_t;
-  mt = mt == -__builtin_inff() ? -3.4028234663852886e38f : mt;
-  const bool group_beaten = fmaf(fabsf(mt), 0x1p-17f, mt) + (slack + 24.f * kLn2) < wbest;
-  if (group_beaten && !TAIL) return;
-  if (TAIL && (group_beaten || e4 >= c1)) return;
+  if (!FIRST) {
+    // group test with the largest bound
+    const float slack = fmaf(fabsf(wbest), 0x1p-17f, 0x1p-12f);
+    float m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(z[0], z[1]),
+                                            __builtin_elementwise_maximum(z[2], z[3]));
+    float mt = m * inv_t;
+    mt = mt == -__builtin_inff() ? -3.4028234663852886e38f : mt;
+    const bool group_beaten = fmaf(fabsf(mt), 0x1p-17f, mt) + (slack + 24.f * kLn2) < wbest;
+    if (group_beaten && !TAIL) return;
+    if (TAIL && (group_beaten || e4 >= c1)) return;
+  }
   unsigned c[4] = {(unsigned)e4 >> 2, node, seq, p.round};
   philox4x32_10(c, p.seed_lo, p.seed_hi);
+  int lead[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) lead[j] = min(__builtin_clrsb((int)c[j]) + 1, 23);  // leading bits equal to the top bit
+  if (FIRST) {
+    int lo_key = (int)0x80000000;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float zt = z[j] * inv_t;
+      const float zt_lo = zt * (zt >= 0.f ? 1.0f - 0x1p-17f : 1.0f + 0x1p-17f);
+      const float g_lo = (int)c[j] < 0 ? (float)(lead[j] - 1) * kLn2 : -2.82f;
+      lo_key = max(lo_key, float_order(__builtin_bit_cast(int, zt_lo + g_lo - 0x1p-12f)));
+    }
+    wbest = __builtin_bit_cast(float, float_order(wave_max_key(lo_key)));
+  }
+  const float slack = fmaf(fabsf(wbest), 0x1p-17f, 0x1p-12f);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     if (TAIL && e4 + j >= c1) break;
     const float zt = z[j] * inv_t;
-    const int lead = min(__builtin_clrsb((int)c[j]) + 1, 23);  // leading bits equal to the top bit
-    const float bound = fmaf((float)lead, kLn2, fmaf(fabsf(zt), 0x1p-17f, zt) + (slack + kLn2));
+    const float bound = fmaf((float)lead[j], kLn2, fmaf(fabsf(zt), 0x1p-17f, zt) + (slack + kLn2));
     if (!(bound < wbest)) {
       const float y = gumbel_logit(z[j], p.temperature, c[j]);
       const int k = order_key(__builtin_bit_cast(unsigned, y));
@@ -401,25 +424,50 @@ __device__ __forceinline__ void sample_group(const AcceptParams& p, const float 
 template <bool BF16, bool VEC>
 __global__ __launch_bounds__(256) void sample_partial(AcceptParams p) {
   __shared__ unsigned long long red[4];
+  __shared__ __align__(16) float s_best[4];  // each wave's running best, shared without barriers
   const int chunk = blockIdx.x % p.chunks;
   const long row = blockIdx.x / p.chunks;
   const unsigned node = (unsigned)(row % p.n_nodes), seq = (unsigned)(row / p.n_nodes);
   const int c0 = chunk * p.chunk_len;  // a multiple of 8: groups of four never straddle chunks
   const int c1 = min(p.vocab, c0 + p.chunk_len);
   const int full_end = c0 + (c1 - c0) / 1024 * 1024;  // iterations where every lane has four tokens
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, wave = tid >> 6;
   const char* rowp = static_cast<const char*>(p.logits) + row * (long)p.vocab * (BF16 ? 2 : 4);
   SampleState st = {(int)0x80000000, 0x7fffffff, -__builtin_inff()};
-  float wbest = -__builtin_inff();  // maximum of lane_best over the wave
+  float wbest = -__builtin_inff();  // a value some token of the workgroup reaches
+  if ((tid & 63) == 0) s_best[wave] = -__builtin_inff();
+  __syncthreads();
+  // A wave publishes its running best to its slot and takes the maximum of
+  // the four slots.  Reads may see another wave's older value: every value a
+  // slot ever holds is reached by some token, so a stale one only skips less.
+  auto share = [&]() __attribute__((always_inline)) {
+    const float wm = __builtin_bit_cast(float, float_order(wave_max_key(float_order(__builtin_bit_cast(int, st.lane_best)))));
+    wbest = wm > wbest ? wm : wbest;  // a NaN maximum leaves wbest as it is
+    if ((tid & 63) == 0) __hip_atomic_store(&s_best[wave], wbest, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    float o = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float x = __hip_atomic_load(&s_best[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      o = x > o ? x : o;
+    }
+    o = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, o)));
+    wbest = o > wbest ? o : wbest;
+  };
   unsigned wn[4] = {0u, 0u, 0u, 0u};
-  if (c0 < full_end) load_group<BF16, VEC>(rowp, c0 + 4 * tid, wn);
-  for (int base = c0; base < full_end; base += 1024) {  // the same trip count for every lane
+  if (c0 < full_end) {
+    load_group<BF16, VEC>(rowp, c0 + 4 * tid, wn);
+    float z[4];
+    unpack_group<BF16, VEC>(wn, z);
+    if (c0 + 1024 < full_end) load_group<BF16, VEC>(rowp, c0 + 1024 + 4 * tid, wn);
+    sample_group<false, true>(p, z, c0 + 4 * tid, c1, node, seq, wbest, st);
+    share();
+  }
+  for (int base = c0 + 1024; base < full_end; base += 1024) {  // the same trip count for every lane
     float z[4];
     unpack_group<BF16, VEC>(wn, z);
     if (base + 1024 < full_end) load_group<BF16, VEC>(rowp, base + 1024 + 4 * tid, wn);
-    sample_group<false>(p, z, base + 4 * tid, c1, node, seq, wbest, st);
-    const float wm = __builtin_bit_cast(float, float_order(wave_max_key(float_order(__builtin_bit_cast(int, st.lane_best)))));
-    wbest = wm > wbest ? wm : wbest;  // a NaN maximum leaves wbest as it is
+    sample_group<false, false>(p, z, base + 4 * tid, c1, node, seq, wbest, st);
+    share();
   }
   if (full_end < c1) {  // the ragged tail: per-token bounds checks
     const int e4 = full_end + 4 * tid;
@@ -429,7 +477,7 @@ __global__ __launch_bounds__(256) void sample_partial(AcceptParams p) {
       z[j] = e4 + j < c1 ? (BF16 ? __builtin_bit_cast(float, (unsigned)reinterpret_cast<const unsigned short*>(rowp)[e4 + j] << 16)
                                  : reinterpret_cast<const float*>(rowp)[e4 + j])
                          : -__builtin_inff();
-    sample_group<true>(p, z, e4, c1, node, seq, wbest, st);
+    sample_group<true, false>(p, z, e4, c1, node, seq, wbest, st);
   }
   unsigned long long w = (st.best_idx == 0x7fffffff) ? 0ull : pack(st.best_key, st.best_idx);
   w = wave_max64(w);

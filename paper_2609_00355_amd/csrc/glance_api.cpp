@@ -227,10 +227,10 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
   chunks = ((long long)vocab + len - 1) / len;
   out->chunks = (int)chunks;
   out->chunk_len = (int)len;
-  // sampling: about 1024 workgroups (four waves a SIMD; measured best of
+  // sampling: about 2048 workgroups (eight waves a SIMD; measured best of
   // 512..4096 at 256 x 152064 bf16), chunks a multiple of 1024 tokens so that
   // only a row's last chunk has a ragged tail
-  long long s_target = 1024;
+  long long s_target = 2048;
   if (const char* e = getenv("GLANCE_SAMPLE_WGS")) {  // tuning override
     const long long v = atoll(e);
     if (v >= 1 && v <= (1 << 20)) s_target = v;

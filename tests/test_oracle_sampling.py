@@ -159,8 +159,10 @@ def test_gumbel_bound_by_leading_zeros():
     k; for u < 1/2 the same expression with L the leading zero bits is >= ln 2,
     above g(1/2) = -ln ln 2.  So (min(L, 23) + 1) ln 2, L the leading bits
     equal to the top bit, bounds the noise from the integer alone, which lets
-    a sampler skip the logarithms of tokens that cannot win.  Checked for
-    every k on the fixed recipe's values, with 2^-16 to spare for its rounding."""
+    a sampler skip the logarithms of tokens that cannot win; (min(L, 23) - 1)
+    ln 2 (u >= 1/2) and -2.82 (u < 1/2) bound it from below, which gives a
+    sampler a running best before any logarithm.  Checked for every k on the
+    fixed recipe's values, with 2^-16 to spare for its rounding."""
     k = np.arange(2 ** 23, dtype=np.uint32)
     u = (k.astype(np.float32) + np.float32(0.5)) * np.float32(2.0 ** -23)
     g = S.gumbel(u).astype(np.float64)
@@ -171,6 +173,11 @@ def test_gumbel_bound_by_leading_zeros():
     lead[nz] = 22 - np.floor(np.log2(flipped[nz].astype(np.float64))).astype(np.int64)
     bound = (np.minimum(lead, 23) + 1) * np.log(2.0)
     assert np.all(g <= bound + 2.0 ** -16)
+    # and from below: for u >= 1/2, -ln u <= (1 - u) / u <= 2 (1 - u), so
+    # g >= -ln 2 - ln(1 - u) >= (min(L, 23) - 1) ln 2; for u < 1/2, g >= g(2^-24) > -2.82
+    top1 = top == 1
+    lower = np.where(top1, (np.minimum(lead, 23) - 1) * np.log(2.0), -2.82)
+    assert np.all(g >= lower)
     # the same bound read as clz(r) - 8 for u >= 1/2
     r = (np.uint32(0x7FFFFF) - k).astype(np.int64)
     hi = top == 1
