@@ -10,7 +10,10 @@ same round is captured once in a HIP graph and replayed.
 Pins: the committed stream equals the target's own greedy autoregressive
 decoding (Thm. 1, decided in fp32), graph replays equal eager rounds, the root
 entropy matches the float64 entropy of the round's root row, and the caches
-end equal to a causal forward's over the committed prefix.  The drafter is a
+end equal to a causal forward's over the committed prefix.  With the sampling
+walk in place of the greedy acceptance (temperatures 1 and 0.5), every round's
+draws and walk equal the oracle's on the round's own verified logits, and the
+caches again equal a causal forward's over what was committed.  The drafter is a
 stand-in (no head weights): N(0,1) logits with the true continuation planted
 at each offset with probability 0.7, so trees accept some tokens and miss
 others.
@@ -22,6 +25,7 @@ import torch
 
 import paper_2609_00355_amd as G
 from oracle import accept as OA
+from oracle import sampling as OS
 
 from gpu_helpers import ensure_lib
 
@@ -118,8 +122,9 @@ def greedy_ar(m, prompt, n):
 class Decoder:
     """Buffers, prepared library calls and the round of one sequence."""
 
-    def __init__(self, m, prompt):
+    def __init__(self, m, prompt, temperature=None, seed=0):
         self.m = m
+        self.temperature, self.seed, self.round_no = temperature, seed, 0
         n = BUDGET + 1
         self.kc = torch.zeros(LAYERS, HKV, CAP, HD, device="cuda")
         self.vc = torch.zeros_like(self.kc)
@@ -145,6 +150,11 @@ class Decoder:
         self.acc = G.glance_greedy_accept(self.logits_buf, self.parents, self.tokens, path_stride=16,
                                           want_entropy=True)
         self.acc_ws = torch.empty(G.glance_accept_workspace_size(1, n, VOCAB), dtype=torch.uint8, device="cuda")
+        if temperature is not None:  # the sampling walk writes draws in place of argmax rows
+            self.acc = {"draws": torch.zeros(1, n, dtype=torch.int32, device="cuda"),
+                        "accept_len": torch.zeros(1, dtype=torch.int32, device="cuda"),
+                        "accept_path": torch.zeros(1, 16, dtype=torch.int32, device="cuda"),
+                        "next_root": torch.zeros(1, dtype=torch.int32, device="cuda")}
         self.k_new = torch.zeros(LAYERS, n, HKV, HD, device="cuda")
         self.v_new = torch.zeros_like(self.k_new)
         self.alen_l = torch.zeros(LAYERS, dtype=torch.int32, device="cuda")
@@ -170,8 +180,12 @@ class Decoder:
                                              self.parents, want_lse=False)
             h = m.mlp(lw, h, o[0])
         self.logits_buf.copy_(m.logits(h)[None])
-        G.glance_greedy_accept(self.logits_buf, self.parents, self.tokens, path_stride=16, outputs=self.acc,
-                               workspace=self.acc_ws, want_entropy=True)  # argmax, walk, root entropy
+        if self.temperature is None:
+            G.glance_greedy_accept(self.logits_buf, self.parents, self.tokens, path_stride=16, outputs=self.acc,
+                                   workspace=self.acc_ws, want_entropy=True)  # argmax, walk, root entropy
+        else:                                                   # draws at temperature T, walk
+            G.glance_sample_accept(self.logits_buf, self.parents, self.tokens, self.temperature, self.seed,
+                                   self.round_no, path_stride=16, outputs=self.acc, workspace=self.acc_ws)
         self.alen_l.copy_(self.acc["accept_len"].expand(LAYERS))
         self.apath_l.copy_(self.acc["accept_path"].expand(LAYERS, 16))
         G.glance_commit_path(self.k_new, self.v_new, self.alen_l, self.apath_l, self.kc, self.vc, self.ctx)
@@ -264,3 +278,43 @@ def test_graph_replays_equal_eager_rounds(setup):
     assert r1 == r2
     for h, ref in ents:
         assert abs(h - ref) <= 2e-4 + 2e-5 * abs(ref)
+
+
+@pytest.mark.parametrize("temperature", [1.0, 0.5])
+def test_sampling_rounds_follow_the_oracle_walk(setup, temperature):
+    """Whole rounds with the sampling walk (eager; the round number is a call
+    argument, so a captured graph would repeat one round's noise): every
+    round's draws, accepted length and path and next root equal the oracle's
+    sampling walk on the GPU's own verified logits, the committed tokens are
+    the walk's, and the caches end equal to a causal pass over the committed
+    prefix."""
+    m, prompt, ar = setup
+    seed = 4242
+    d = Decoder(m, prompt, temperature=temperature, seed=seed)
+    committed = [int(d.root[0])]
+    accepted = 0
+    while int(d.count.item()) < N_GEN:
+        d.set_draft(ar, prompt, seed=d.round_no)
+        d.round()
+        torch.cuda.synchronize()
+        rows = d.logits_buf[0].cpu().numpy()
+        par, tok = d.parents[0].cpu().tolist(), d.tokens[0].cpu().tolist()
+        draws, a, path, nr = OS.sampling_walk(rows, par, tok, temperature, seed, d.round_no, 0)
+        assert d.acc["draws"][0].cpu().tolist() == draws, d.round_no
+        assert int(d.acc["accept_len"][0]) == a
+        assert d.acc["accept_path"][0].cpu().tolist()[:a + 1] == list(path)
+        assert int(d.acc["next_root"][0]) == nr
+        committed += [tok[c] for c in path[1:]] + [nr]
+        accepted += a
+        d.round_no += 1
+        assert d.round_no < 200
+    out = d.out[:N_GEN].cpu().tolist()
+    assert out == committed[:N_GEN]
+    assert accepted > 0                                          # some drafted tokens were drawn and kept
+    ctx = int(d.ctx[0])
+    assert ctx == PROMPT + int(d.count.item()) - 1
+    _, kv = m.forward_causal(prompt + committed[:ctx - PROMPT])
+    for li, (k, v) in enumerate(kv):
+        torch.testing.assert_close(d.kc[li, :, :ctx], k.transpose(0, 1), rtol=1e-4, atol=1e-4)
+        torch.testing.assert_close(d.vc[li, :, :ctx], v.transpose(0, 1), rtol=1e-4, atol=1e-4)
+    print(f"[T={temperature}] rounds={d.round_no} accepted={accepted}", flush=True)
