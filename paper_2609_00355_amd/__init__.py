@@ -266,7 +266,8 @@ def glance_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None
     return outputs
 
 
-def _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream, want_entropy):
+def _accept_common(logits, parents, tokens, path_stride, outputs, workspace, rows_key):
+    """Checks and outputs shared by both acceptances; `rows_key` names the per-row output."""
     torch = _torch()
     _dev(logits, "logits", ndim=3)
     code = _dtype_code(logits)
@@ -279,22 +280,31 @@ def _accept_args(logits, parents, tokens, path_stride, outputs, workspace, strea
     dev = logits.device
     if outputs is None:
         outputs = {
-            "argmax": torch.empty((batch, n), dtype=torch.int32, device=dev),
+            rows_key: torch.empty((batch, n), dtype=torch.int32, device=dev),
             "accept_len": torch.empty((batch,), dtype=torch.int32, device=dev),
             "accept_path": torch.empty((batch, path_stride), dtype=torch.int32, device=dev),
             "next_root": torch.empty((batch,), dtype=torch.int32, device=dev),
         }
-    if want_entropy and outputs.get("root_entropy") is None:
-        outputs["root_entropy"] = torch.empty((batch,), dtype=torch.float32, device=dev)
     need = glance_accept_workspace_size(batch, n, vocab)
     if need == 0:
         raise GlanceError(GLANCE_ERR_INVALID_ARG, glance_last_error())
     ws = _workspace(need, dev, workspace)
-    args = [ctypes.c_int32(batch), ctypes.c_int32(n), ctypes.c_int32(vocab), ctypes.c_int(code), _ptr(logits),
-            _ptr(parents), _ptr(tokens), _ptr(outputs["argmax"]), _ptr(outputs["accept_len"]),
-            _ptr(outputs["accept_path"]), ctypes.c_int32(path_stride), _ptr(outputs["next_root"]),
-            _ptr(outputs.get("root_entropy")), _ptr(ws), ctypes.c_size_t(ws.numel() * ws.element_size()),
-            _stream(stream)]
+    head = [ctypes.c_int32(batch), ctypes.c_int32(n), ctypes.c_int32(vocab), ctypes.c_int(code), _ptr(logits),
+            _ptr(parents), _ptr(tokens)]
+    walk = [_ptr(outputs["accept_len"]), _ptr(outputs["accept_path"]), ctypes.c_int32(path_stride),
+            _ptr(outputs["next_root"])]
+    tail = [_ptr(ws), ctypes.c_size_t(ws.numel() * ws.element_size())]
+    return head, walk, tail, outputs, ws
+
+
+def _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream, want_entropy):
+    torch = _torch()
+    head, walk, tail, outputs, ws = _accept_common(logits, parents, tokens, path_stride, outputs, workspace,
+                                                   "argmax")
+    if want_entropy and outputs.get("root_entropy") is None:
+        outputs["root_entropy"] = torch.empty((logits.shape[0],), dtype=torch.float32, device=logits.device)
+    args = head + [_ptr(outputs["argmax"])] + walk + [_ptr(outputs.get("root_entropy"))] + tail + \
+        [_stream(stream)]
     return args, outputs, ws
 
 
@@ -311,18 +321,13 @@ def glance_sample_accept(logits, parents, tokens, temperature, seed, round_, pat
 
 
 def _sample_args(logits, parents, tokens, temperature, seed, round_, path_stride, outputs, workspace, stream):
-    torch = _torch()
     seed, round_ = int(seed), int(round_)
     if not 0 <= seed < 2 ** 64 or not 0 <= round_ < 2 ** 32:
         raise ValueError("seed must fit 64 bits and round_ 32 bits, both unsigned")
-    if outputs is not None and "draws" in outputs:
-        outputs = dict(outputs, argmax=outputs["draws"])
-    args, outputs, _ = _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream, False)
-    # glance_greedy_accept's argument list with the row results renamed to draws
-    # and (temperature, seed, round) in place of the root-entropy pointer
-    outputs["draws"] = outputs.pop("argmax")
-    args = args[:7] + [ctypes.c_float(float(temperature)), ctypes.c_uint64(seed), ctypes.c_uint32(round_)] + \
-        args[7:12] + args[13:]
+    head, walk, tail, outputs, _ = _accept_common(logits, parents, tokens, path_stride, outputs, workspace,
+                                                  "draws")
+    args = head + [ctypes.c_float(float(temperature)), ctypes.c_uint64(seed), ctypes.c_uint32(round_),
+                   _ptr(outputs["draws"])] + walk + tail + [_stream(stream)]
     return args, outputs
 
 

@@ -339,14 +339,14 @@ glance_status glance_tree_verify_attn(const glance_attn_shape* s, const void* q,
                      workspace_bytes, stream);
 }
 
-glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
-                                   glance_dtype logits_dtype, const void* logits,
-                                   const int32_t* parents, const int32_t* tokens,
-                                   int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
-                                   int32_t path_stride, int32_t* next_root, float* root_entropy,
-                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  AcceptPlan pl;
-  glance_status st = accept_plan(batch, n_nodes, vocab, &pl);
+// Host checks and parameters shared by the greedy and the sampling
+// acceptance; `rows_name` names the per-row output in error messages.
+glance_status accept_setup(int32_t batch, int32_t n_nodes, int32_t vocab, glance_dtype logits_dtype,
+                           const void* logits, const int32_t* parents, const int32_t* tokens,
+                           int32_t* rows_out, const char* rows_name, int32_t* accept_len,
+                           int32_t* accept_path, int32_t path_stride, int32_t* next_root, void* workspace,
+                           size_t workspace_bytes, AcceptPlan* pl, glance::AcceptParams* p) {
+  glance_status st = accept_plan(batch, n_nodes, vocab, pl);
   if (st != GLANCE_OK) return st;
   if (logits_dtype != GLANCE_F32 && logits_dtype != GLANCE_BF16)
     return fail(GLANCE_ERR_UNSUPPORTED, "logits dtype must be GLANCE_F32 or GLANCE_BF16");
@@ -355,7 +355,7 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
     const void* ptr;
     const char* name;
   } req[] = {{logits, "logits"},         {parents, "parents"},         {tokens, "tokens"},
-             {argmax_out, "argmax_out"}, {accept_len, "accept_len"}, {accept_path, "accept_path"},
+             {rows_out, rows_name},      {accept_len, "accept_len"}, {accept_path, "accept_path"},
              {next_root, "next_root"}};
   for (auto& r : req) {
     if (!r.ptr) return fail(GLANCE_ERR_INVALID_ARG, "%s is NULL", r.name);
@@ -363,29 +363,44 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
   }
   if (logits_dtype == GLANCE_BF16 && (reinterpret_cast<uintptr_t>(logits) & 1u))
     return fail(GLANCE_ERR_INVALID_ARG, "logits is not 2-byte aligned");
-  if (root_entropy && (reinterpret_cast<uintptr_t>(root_entropy) & 3u))
-    return fail(GLANCE_ERR_INVALID_ARG, "root_entropy is not 4-byte aligned");
   if (!workspace) return fail(GLANCE_ERR_WORKSPACE, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(GLANCE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-  if (workspace_bytes < pl.bytes)
+  if (workspace_bytes < pl->bytes)
     return fail(GLANCE_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes,
-                pl.bytes);
-  glance::AcceptParams p = {};
-  p.logits = logits;
-  p.parents = parents;
-  p.tokens = tokens;
-  p.argmax_out = argmax_out;
-  p.accept_len = accept_len;
-  p.accept_path = accept_path;
-  p.next_root = next_root;
+                pl->bytes);
+  *p = glance::AcceptParams{};
+  p->logits = logits;
+  p->parents = parents;
+  p->tokens = tokens;
+  p->argmax_out = rows_out;
+  p->accept_len = accept_len;
+  p->accept_path = accept_path;
+  p->next_root = next_root;
+  p->part = static_cast<unsigned long long*>(workspace);
+  p->ent_part = reinterpret_cast<float4*>(static_cast<char*>(workspace) + pl->part_bytes);
+  p->batch = batch;
+  p->n_nodes = n_nodes;
+  p->vocab = vocab;
+  p->path_stride = path_stride;
+  return ok();
+}
+
+glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                   glance_dtype logits_dtype, const void* logits,
+                                   const int32_t* parents, const int32_t* tokens,
+                                   int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
+                                   int32_t path_stride, int32_t* next_root, float* root_entropy,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  AcceptPlan pl;
+  glance::AcceptParams p;
+  glance_status st = accept_setup(batch, n_nodes, vocab, logits_dtype, logits, parents, tokens, argmax_out,
+                                  "argmax_out", accept_len, accept_path, path_stride, next_root, workspace,
+                                  workspace_bytes, &pl, &p);
+  if (st != GLANCE_OK) return st;
+  if (root_entropy && (reinterpret_cast<uintptr_t>(root_entropy) & 3u))
+    return fail(GLANCE_ERR_INVALID_ARG, "root_entropy is not 4-byte aligned");
   p.root_entropy = root_entropy;
-  p.part = static_cast<unsigned long long*>(workspace);
-  p.ent_part = reinterpret_cast<float4*>(static_cast<char*>(workspace) + pl.part_bytes);
-  p.batch = batch;
-  p.n_nodes = n_nodes;
-  p.vocab = vocab;
-  p.path_stride = path_stride;
   p.chunks = pl.chunks;
   p.chunk_len = pl.chunk_len;
   hipEvent_t e0, e1;
@@ -402,45 +417,14 @@ glance_status glance_sample_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    int32_t* next_root, void* workspace, size_t workspace_bytes,
                                    hipStream_t stream) {
   AcceptPlan pl;
-  glance_status st = accept_plan(batch, n_nodes, vocab, &pl);
+  glance::AcceptParams p;
+  glance_status st = accept_setup(batch, n_nodes, vocab, logits_dtype, logits, parents, tokens, draws_out,
+                                  "draws_out", accept_len, accept_path, path_stride, next_root, workspace,
+                                  workspace_bytes, &pl, &p);
   if (st != GLANCE_OK) return st;
-  if (logits_dtype != GLANCE_F32 && logits_dtype != GLANCE_BF16)
-    return fail(GLANCE_ERR_UNSUPPORTED, "logits dtype must be GLANCE_F32 or GLANCE_BF16");
   if (!(temperature >= FLT_MIN) || !(temperature <= FLT_MAX))
     return fail(GLANCE_ERR_INVALID_ARG, "temperature must be a finite normal float > 0 (got %g)",
                 (double)temperature);
-  if (path_stride < 1) return fail(GLANCE_ERR_INVALID_ARG, "path_stride must be >= 1");
-  struct {
-    const void* ptr;
-    const char* name;
-  } req[] = {{logits, "logits"},       {parents, "parents"},         {tokens, "tokens"},
-             {draws_out, "draws_out"}, {accept_len, "accept_len"}, {accept_path, "accept_path"},
-             {next_root, "next_root"}};
-  for (auto& r : req) {
-    if (!r.ptr) return fail(GLANCE_ERR_INVALID_ARG, "%s is NULL", r.name);
-    if (reinterpret_cast<uintptr_t>(r.ptr) & 3u) return fail(GLANCE_ERR_INVALID_ARG, "%s is not 4-byte aligned", r.name);
-  }
-  if (logits_dtype == GLANCE_BF16 && (reinterpret_cast<uintptr_t>(logits) & 1u))
-    return fail(GLANCE_ERR_INVALID_ARG, "logits is not 2-byte aligned");
-  if (!workspace) return fail(GLANCE_ERR_WORKSPACE, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
-    return fail(GLANCE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-  if (workspace_bytes < pl.bytes)
-    return fail(GLANCE_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes,
-                pl.bytes);
-  glance::AcceptParams p = {};
-  p.logits = logits;
-  p.parents = parents;
-  p.tokens = tokens;
-  p.argmax_out = draws_out;
-  p.accept_len = accept_len;
-  p.accept_path = accept_path;
-  p.next_root = next_root;
-  p.part = static_cast<unsigned long long*>(workspace);
-  p.batch = batch;
-  p.n_nodes = n_nodes;
-  p.vocab = vocab;
-  p.path_stride = path_stride;
   p.chunks = pl.sample_chunks;
   p.chunk_len = pl.sample_chunk_len;
   p.temperature = temperature;
