@@ -206,6 +206,13 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
  *                glance_greedy_accept
  *   seed, round  the generator's key and the round number (callers advance
  *                round every round so that draws never repeat)
+ *   round_counter device uint32, or NULL: when given, the round number used
+ *                is round + *round_counter (read before any draw), and the
+ *                call adds 1 to *round_counter after its draws, in stream
+ *                order.  A HIP graph that captures the call then draws fresh
+ *                noise on every replay (a captured by-value round would
+ *                repeat one round's noise).  Calls sharing a counter must be
+ *                ordered on one stream.
  *   draws_out    device [batch][n_nodes] int32: each row's draw
  *   other arguments, shapes, output layouts and the workspace: as for
  *   glance_greedy_accept (glance_accept_workspace_size); no root entropy.
@@ -215,7 +222,7 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
 glance_status glance_sample_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
                                    glance_dtype logits_dtype, const void* logits,
                                    const int32_t* parents, const int32_t* tokens, float temperature,
-                                   uint64_t seed, uint32_t round, int32_t* draws_out,
+                                   uint64_t seed, uint32_t round, uint32_t* round_counter, int32_t* draws_out,
                                    int32_t* accept_len, int32_t* accept_path, int32_t path_stride,
                                    int32_t* next_root, void* workspace, size_t workspace_bytes,
                                    hipStream_t stream);

@@ -59,8 +59,8 @@ _SIGS = {
     "glance_greedy_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P, _P, _I32,
                                             _P, _P, _P, _SZ, _P]),
     "glance_sample_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, ctypes.c_float,
-                                            ctypes.c_uint64, ctypes.c_uint32, _P, _P, _P, _I32, _P, _P, _SZ,
-                                            _P]),
+                                            ctypes.c_uint64, ctypes.c_uint32, _P, _P, _P, _P, _I32, _P, _P,
+                                            _SZ, _P]),
     "glance_build_tree": (ctypes.c_int, [_I32, _I32, _I32, _I32, ctypes.c_int, _P, ctypes.c_int64, _P, _P,
                                          _P, _P, _P, _SZ, _P]),
     "glance_tree_workspace_size": (_SZ, [_I32, _I32, _I32, _I32]),
@@ -309,25 +309,33 @@ def _accept_args(logits, parents, tokens, path_stride, outputs, workspace, strea
 
 
 def glance_sample_accept(logits, parents, tokens, temperature, seed, round_, path_stride=None, outputs=None,
-                         workspace=None, stream=None):
+                         workspace=None, stream=None, round_counter=None):
     """Row draws from softmax(z / temperature) (Gumbel-max over Philox4x32-10
     noise keyed by seed, counted by round) + the walk of Algorithm 1 over the
     draws.  Returns a dict of int32 GPU tensors: draws, accept_len,
-    accept_path, next_root."""
+    accept_path, next_root.  round_counter: optional one-element int32 GPU
+    tensor read as unsigned; the round used is round_ + its value, and the
+    call advances it by one (for graph replays that draw fresh noise)."""
     args, outputs = _sample_args(logits, parents, tokens, temperature, seed, round_, path_stride, outputs,
-                                 workspace, stream)
+                                 workspace, stream, round_counter)
     _check(lib().glance_sample_accept(*args))
     return outputs
 
 
-def _sample_args(logits, parents, tokens, temperature, seed, round_, path_stride, outputs, workspace, stream):
+def _sample_args(logits, parents, tokens, temperature, seed, round_, path_stride, outputs, workspace, stream,
+                 round_counter=None):
+    torch = _torch()
     seed, round_ = int(seed), int(round_)
     if not 0 <= seed < 2 ** 64 or not 0 <= round_ < 2 ** 32:
         raise ValueError("seed must fit 64 bits and round_ 32 bits, both unsigned")
+    if round_counter is not None:
+        _dev(round_counter, "round_counter", torch.int32, 1)
+        if round_counter.numel() != 1:
+            raise ValueError("round_counter must hold one element")
     head, walk, tail, outputs, _ = _accept_common(logits, parents, tokens, path_stride, outputs, workspace,
                                                   "draws")
     args = head + [ctypes.c_float(float(temperature)), ctypes.c_uint64(seed), ctypes.c_uint32(round_),
-                   _ptr(outputs["draws"])] + walk + tail + [_stream(stream)]
+                   _ptr(round_counter), _ptr(outputs["draws"])] + walk + tail + [_stream(stream)]
     return args, outputs
 
 

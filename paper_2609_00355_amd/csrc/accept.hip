@@ -373,7 +373,8 @@ struct SampleState {
 // skipped, so the exact draw is kept.
 template <bool TAIL, bool FIRST>
 __device__ __forceinline__ void sample_group(const AcceptParams& p, const float (&z)[4], int e4, int c1,
-                                             unsigned node, unsigned seq, float& wbest, SampleState& st) {
+                                             unsigned node, unsigned seq, unsigned rnd, float& wbest,
+                                             SampleState& st) {
   constexpr float kLn2 = 0.6931472f;
   const float inv_t = p.inv_temperature;
   if (!FIRST) {
@@ -387,7 +388,7 @@ __device__ __forceinline__ void sample_group(const AcceptParams& p, const float 
     if (group_beaten && !TAIL) return;
     if (TAIL && (group_beaten || e4 >= c1)) return;
   }
-  unsigned c[4] = {(unsigned)e4 >> 2, node, seq, p.round};
+  unsigned c[4] = {(unsigned)e4 >> 2, node, seq, rnd};
   philox4x32_10(c, p.seed_lo, p.seed_hi);
   int lead[4];
 #pragma unroll
@@ -433,6 +434,11 @@ __global__ __launch_bounds__(256) void sample_partial(AcceptParams p) {
   const int full_end = c0 + (c1 - c0) / 1024 * 1024;  // iterations where every lane has four tokens
   const int tid = threadIdx.x, wave = tid >> 6;
   const char* rowp = static_cast<const char*>(p.logits) + row * (long)p.vocab * (BF16 ? 2 : 4);
+  // the round number: the argument, plus the device counter when one is given
+  // (the walk kernel, later on the stream, advances it)
+  const unsigned rnd = p.round + (p.round_counter ? __hip_atomic_load(p.round_counter, __ATOMIC_RELAXED,
+                                                                      __HIP_MEMORY_SCOPE_AGENT)
+                                                  : 0u);
   SampleState st = {(int)0x80000000, 0x7fffffff, -__builtin_inff()};
   float wbest = -__builtin_inff();  // a value some token of the workgroup reaches
   if ((tid & 63) == 0) s_best[wave] = -__builtin_inff();
@@ -459,14 +465,14 @@ __global__ __launch_bounds__(256) void sample_partial(AcceptParams p) {
     float z[4];
     unpack_group<BF16, VEC>(wn, z);
     if (c0 + 1024 < full_end) load_group<BF16, VEC>(rowp, c0 + 1024 + 4 * tid, wn);
-    sample_group<false, true>(p, z, c0 + 4 * tid, c1, node, seq, wbest, st);
+    sample_group<false, true>(p, z, c0 + 4 * tid, c1, node, seq, rnd, wbest, st);
     share();
   }
   for (int base = c0 + 1024; base < full_end; base += 1024) {  // the same trip count for every lane
     float z[4];
     unpack_group<BF16, VEC>(wn, z);
     if (base + 1024 < full_end) load_group<BF16, VEC>(rowp, base + 1024 + 4 * tid, wn);
-    sample_group<false, false>(p, z, base + 4 * tid, c1, node, seq, wbest, st);
+    sample_group<false, false>(p, z, base + 4 * tid, c1, node, seq, rnd, wbest, st);
     share();
   }
   if (full_end < c1) {  // the ragged tail: per-token bounds checks
@@ -477,7 +483,7 @@ __global__ __launch_bounds__(256) void sample_partial(AcceptParams p) {
       z[j] = e4 + j < c1 ? (BF16 ? __builtin_bit_cast(float, (unsigned)reinterpret_cast<const unsigned short*>(rowp)[e4 + j] << 16)
                                  : reinterpret_cast<const float*>(rowp)[e4 + j])
                          : -__builtin_inff();
-    sample_group<true, false>(p, z, e4, c1, node, seq, wbest, st);
+    sample_group<true, false>(p, z, e4, c1, node, seq, rnd, wbest, st);
   }
   unsigned long long w = (st.best_idx == 0x7fffffff) ? 0ull : pack(st.best_key, st.best_idx);
   w = wave_max64(w);
@@ -527,6 +533,12 @@ __global__ __launch_bounds__(64) void accept_walk(AcceptParams p) {
   if (lane == 0) {
     p.accept_len[b] = len;
     p.next_root[b] = sAm[v];
+  }
+  // sampling with a device round counter: every row draw of this call has
+  // read it (the draws kernel ran earlier on the stream), so advance it once
+  if (p.round_counter && b == 0 && lane == 0) {
+    const unsigned r = __hip_atomic_load(p.round_counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p.round_counter, r + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (p.root_entropy && lane == 0) {
     // merge the chunks relative to the row maximum M:

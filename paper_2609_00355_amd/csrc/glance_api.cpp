@@ -412,7 +412,7 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
 glance_status glance_sample_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
                                    glance_dtype logits_dtype, const void* logits,
                                    const int32_t* parents, const int32_t* tokens, float temperature,
-                                   uint64_t seed, uint32_t round, int32_t* draws_out,
+                                   uint64_t seed, uint32_t round, uint32_t* round_counter, int32_t* draws_out,
                                    int32_t* accept_len, int32_t* accept_path, int32_t path_stride,
                                    int32_t* next_root, void* workspace, size_t workspace_bytes,
                                    hipStream_t stream) {
@@ -431,7 +431,10 @@ glance_status glance_sample_accept(int32_t batch, int32_t n_nodes, int32_t vocab
   p.inv_temperature = 1.0f / temperature;
   p.seed_lo = (unsigned)(seed & 0xffffffffu);
   p.seed_hi = (unsigned)(seed >> 32);
+  if (round_counter && (reinterpret_cast<uintptr_t>(round_counter) & 3u))
+    return fail(GLANCE_ERR_INVALID_ARG, "round_counter is not 4-byte aligned");
   p.round = round;
+  p.round_counter = round_counter;
   hipEvent_t e0, e1;
   take_events(&e0, &e1);
   return check_hip(glance::launch_sample(p, logits_dtype == GLANCE_BF16, stream, e0, e1),

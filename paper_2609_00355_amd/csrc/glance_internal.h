@@ -65,6 +65,7 @@ struct AcceptParams {
   // sampling walk only: the row draws are argmax(z / temperature + Gumbel)
   float temperature, inv_temperature;
   unsigned seed_lo, seed_hi, round;
+  unsigned* round_counter;   // or null: added to round, then advanced by the walk
 };
 
 // Draft tree builder.  Limits: budget N <= kTreeMaxBudget strings below the

@@ -128,9 +128,10 @@ def test_accept_argument_checks(lib):
     assert st == G.GLANCE_ERR_WORKSPACE
 
 
-def _sample(lib, n=8, temperature=1.0, parents=FAKE, draws=FAKE, ws=FAKE, ws_bytes=1 << 20, dtype=G.GLANCE_BF16):
+def _sample(lib, n=8, temperature=1.0, parents=FAKE, draws=FAKE, ws=FAKE, ws_bytes=1 << 20, dtype=G.GLANCE_BF16,
+            counter=None):
     return lib.glance_sample_accept(1, n, 100, dtype, FAKE, parents, FAKE, temperature, 2 ** 64 - 1, 2 ** 32 - 1,
-                                    draws, FAKE, FAKE, 8, FAKE, ws, ws_bytes, None)
+                                    counter, draws, FAKE, FAKE, 8, FAKE, ws, ws_bytes, None)
 
 
 def test_sample_argument_checks(lib):
@@ -143,6 +144,8 @@ def test_sample_argument_checks(lib):
     assert _sample(lib, ws_bytes=1) == G.GLANCE_ERR_WORKSPACE
     assert _sample(lib, ws=ctypes.c_void_p(0x10010)) == G.GLANCE_ERR_WORKSPACE
     assert _sample(lib, dtype=7) == G.GLANCE_ERR_UNSUPPORTED
+    assert _sample(lib, counter=ctypes.c_void_p(0x10002)) == G.GLANCE_ERR_INVALID_ARG
+    assert "round_counter" in G.glance_last_error()
 
 
 def _build_tree(lib, batch=1, horizon=15, vocab=152064, budget=63, dtype=G.GLANCE_BF16, logits=FAKE,

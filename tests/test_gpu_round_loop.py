@@ -122,9 +122,12 @@ def greedy_ar(m, prompt, n):
 class Decoder:
     """Buffers, prepared library calls and the round of one sequence."""
 
-    def __init__(self, m, prompt, temperature=None, seed=0):
+    def __init__(self, m, prompt, temperature=None, seed=0, device_round=False):
         self.m = m
         self.temperature, self.seed, self.round_no = temperature, seed, 0
+        # with device_round the sampling call reads and advances a device
+        # counter, so a captured round draws fresh noise on every replay
+        self.round_counter = torch.zeros(1, dtype=torch.int32, device="cuda") if device_round else None
         n = BUDGET + 1
         self.kc = torch.zeros(LAYERS, HKV, CAP, HD, device="cuda")
         self.vc = torch.zeros_like(self.kc)
@@ -185,7 +188,8 @@ class Decoder:
                                    workspace=self.acc_ws, want_entropy=True)  # argmax, walk, root entropy
         else:                                                   # draws at temperature T, walk
             G.glance_sample_accept(self.logits_buf, self.parents, self.tokens, self.temperature, self.seed,
-                                   self.round_no, path_stride=16, outputs=self.acc, workspace=self.acc_ws)
+                                   0 if self.round_counter is not None else self.round_no, path_stride=16,
+                                   outputs=self.acc, workspace=self.acc_ws, round_counter=self.round_counter)
         self.alen_l.copy_(self.acc["accept_len"].expand(LAYERS))
         self.apath_l.copy_(self.acc["accept_path"].expand(LAYERS, 16))
         G.glance_commit_path(self.k_new, self.v_new, self.alen_l, self.apath_l, self.kc, self.vc, self.ctx)
@@ -198,6 +202,14 @@ class Decoder:
         self.out.index_put_((idx,), torch.where(keep, toks.int(), self.out[idx]))
         self.count += a + 1
         self.root.copy_(self.acc["next_root"])
+
+    def set_draft_tokens(self, cont, seed):
+        """The stand-in drafter planting the given continuation of the root at every offset."""
+        rng = np.random.default_rng(seed)
+        z = rng.normal(size=(L_DRAFT, VOCAB)).astype(np.float32)
+        for j, t in enumerate(cont[:L_DRAFT]):
+            z[j, t] = 8.0
+        self.draft.copy_(torch.from_numpy(z)[None])
 
     def set_draft(self, ar_stream, prompt, seed):
         """The stand-in drafter: N(0,1) logits, the true continuation planted with p = 0.7."""
@@ -280,23 +292,42 @@ def test_graph_replays_equal_eager_rounds(setup):
         assert abs(h - ref) <= 2e-4 + 2e-5 * abs(ref)
 
 
-@pytest.mark.parametrize("temperature", [1.0, 0.5])
-def test_sampling_rounds_follow_the_oracle_walk(setup, temperature):
-    """Whole rounds with the sampling walk (eager; the round number is a call
-    argument, so a captured graph would repeat one round's noise): every
+@pytest.mark.parametrize("temperature,graph", [(1.0, False), (0.5, False), (1.0, True)])
+def test_sampling_rounds_follow_the_oracle_walk(setup, temperature, graph):
+    """Whole rounds with the sampling walk, eagerly with the round number as a
+    call argument, or captured once in a HIP graph and replayed with a device
+    round counter (so each replay draws the next round's noise): every
     round's draws, accepted length and path and next root equal the oracle's
     sampling walk on the GPU's own verified logits, the committed tokens are
     the walk's, and the caches end equal to a causal pass over the committed
     prefix."""
     m, prompt, ar = setup
     seed = 4242
-    d = Decoder(m, prompt, temperature=temperature, seed=seed)
+    d = Decoder(m, prompt, temperature=temperature, seed=seed, device_round=graph)
     committed = [int(d.root[0])]
     accepted = 0
+    g = None
     while int(d.count.item()) < N_GEN:
-        d.set_draft(ar, prompt, seed=d.round_no)
-        d.round()
+        # the drafter proposes the greedy continuation of what was committed so
+        # far (the root included), which draws at these temperatures often follow
+        cont, _ = greedy_ar(m, prompt + committed, L_DRAFT)
+        d.set_draft_tokens(cont, seed=d.round_no)
+        if graph and g is None and d.round_no == 1:            # capture after one eager round
+            torch.cuda.synchronize()
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                d.round()
+            torch.cuda.synchronize()
+            g.replay()
+        elif g is not None:
+            g.replay()
+        else:
+            d.round()
         torch.cuda.synchronize()
+        if graph:
+            assert int(d.round_counter.item()) == d.round_no + 1
         rows = d.logits_buf[0].cpu().numpy()
         par, tok = d.parents[0].cpu().tolist(), d.tokens[0].cpu().tolist()
         draws, a, path, nr = OS.sampling_walk(rows, par, tok, temperature, seed, d.round_no, 0)
@@ -310,11 +341,11 @@ def test_sampling_rounds_follow_the_oracle_walk(setup, temperature):
         assert d.round_no < 200
     out = d.out[:N_GEN].cpu().tolist()
     assert out == committed[:N_GEN]
-    assert accepted > 0                                          # some drafted tokens were drawn and kept
+    assert accepted >= 10                                        # drafted tokens were drawn and kept
     ctx = int(d.ctx[0])
     assert ctx == PROMPT + int(d.count.item()) - 1
     _, kv = m.forward_causal(prompt + committed[:ctx - PROMPT])
     for li, (k, v) in enumerate(kv):
         torch.testing.assert_close(d.kc[li, :, :ctx], k.transpose(0, 1), rtol=1e-4, atol=1e-4)
         torch.testing.assert_close(d.vc[li, :, :ctx], v.transpose(0, 1), rtol=1e-4, atol=1e-4)
-    print(f"[T={temperature}] rounds={d.round_no} accepted={accepted}", flush=True)
+    print(f"[T={temperature} graph={graph}] rounds={d.round_no} accepted={accepted}", flush=True)

@@ -219,3 +219,39 @@ def test_host_checks():
             G.glance_sample_accept(logits, par, tok, bad, 0, 0)
     with pytest.raises(ValueError):
         G.glance_sample_accept(logits, par, tok, 1.0, -1, 0)
+
+
+def test_device_round_counter_gives_fresh_noise_on_graph_replays():
+    """With a device round counter the round used is round_ + counter and the
+    call advances the counter: eager calls and the replays of a captured HIP
+    graph each draw the next round's noise (checked against the oracle at
+    that round), with the program's own synchronisation between replays."""
+    logits, par, tok = _peaked(2, 8, 3000, seed=12, dtype=torch.bfloat16, peak=3.0)
+    dl, dp, dt = logits.cuda(), par.cuda(), tok.cuda()
+    base, seed = 100, 5
+    counter = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(G.glance_accept_workspace_size(2, 8, 3000), dtype=torch.uint8, device="cuda")
+    out = G.glance_sample_accept(dl, dp, dt, 1.0, seed, base, path_stride=16, workspace=ws, round_counter=counter)
+    torch.cuda.synchronize()
+    assert int(counter.item()) == 1
+    _check({k: v.cpu().numpy() for k, v in out.items()}, logits, par, tok, 1.0, seed, base)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        G.glance_sample_accept(dl, dp, dt, 1.0, seed, base, path_stride=16, outputs=out, workspace=ws,
+                               round_counter=counter)
+    torch.cuda.synchronize()
+    assert int(counter.item()) == 1                          # capture records, it does not run
+    seen = []
+    for r in range(1, 5):
+        g.replay()
+        torch.cuda.synchronize()
+        got = {k: v.cpu().numpy() for k, v in out.items()}
+        _check(got, logits, par, tok, 1.0, seed, base + r)
+        assert int(counter.item()) == r + 1
+        seen.append(got["draws"].copy())
+    assert any((a != b).any() for a, b in zip(seen, seen[1:]))
+    # without a counter the same by-value round gives the same draws
+    a = _run(logits, par, tok, 1.0, seed, base + 3)
+    assert np.array_equal(a["draws"], seen[2])
