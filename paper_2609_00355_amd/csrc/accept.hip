@@ -468,12 +468,16 @@ __global__ __launch_bounds__(256) void sample_partial(AcceptParams p) {
     sample_group<false, true>(p, z, c0 + 4 * tid, c1, node, seq, rnd, wbest, st);
     share();
   }
+  // the running best is exchanged every iteration while it still climbs fast,
+  // then every fourth (a uniform condition: the exchange needs every lane)
+  int it = 0;
   for (int base = c0 + 1024; base < full_end; base += 1024) {  // the same trip count for every lane
     float z[4];
     unpack_group<BF16, VEC>(wn, z);
     if (base + 1024 < full_end) load_group<BF16, VEC>(rowp, base + 1024 + 4 * tid, wn);
     sample_group<false, false>(p, z, base + 4 * tid, c1, node, seq, rnd, wbest, st);
-    share();
+    ++it;
+    if (it <= 4 || (it & 3) == 0) share();
   }
   if (full_end < c1) {  // the ragged tail: per-token bounds checks
     const int e4 = full_end + 4 * tid;
