@@ -507,13 +507,22 @@ __global__ __launch_bounds__(64) void accept_walk(AcceptParams p) {
   int par = -1;
   int tok = 0;
   if (lane < n) {
-    unsigned long long w = 0ull;
-    const unsigned long long* src = p.part + (rb + lane) * p.chunks;
-    for (int c = 0; c < p.chunks; ++c) w = umax64(w, src[c]);
-    am = (int)(0xffffffffu - (unsigned int)(w & 0xffffffffull));
-    p.argmax_out[rb + lane] = am;
+    // the tree and the chunk words are all loaded before any is used (one
+    // memory round trip; the argmax store below could alias the tree inputs,
+    // so the compiler would not hoist their loads over it)
     par = p.parents[rb + lane];
     tok = p.tokens[rb + lane];
+    unsigned long long w = 0ull;
+    const unsigned long long* src = p.part + (rb + lane) * p.chunks;
+    for (int c0 = 0; c0 < p.chunks; c0 += 8) {
+      unsigned long long v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = c0 + u < p.chunks ? src[c0 + u] : 0ull;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) w = umax64(w, v[u]);
+    }
+    am = (int)(0xffffffffu - (unsigned int)(w & 0xffffffffull));
+    p.argmax_out[rb + lane] = am;
     sAm[lane] = am;
   }
   __syncthreads();
