@@ -347,10 +347,10 @@ __device__ __forceinline__ void unpack_group(const unsigned (&w)[4], float (&z)[
 // tested against the wave's running best y* (the largest z / T + g found so
 // far by any lane of the wave) with an upper bound on its noise read off the
 // uniform's integer: with u = (k + 0.5) 2^-23, r = 2^23 - 1 - k and x the
-// generator word (k = x >> 9), g <= -ln(1 - u) <= (clz(r) - 8) ln 2, and
-// clz(r) - 8 = min(L, 23) + 1 when u >= 1/2, L being the leading one bits of
-// x (v_ffbh_i32); for u < 1/2 the same expression is >= ln 2 > g(1/2).  The
-// fixed recipe stays within 1e-7 of this bound.  A token is skipped only when
+// generator word (k = x >> 9), g <= -ln(1 - u) <= (23 - log2 r) ln 2, and
+// log2 r >= F 2^-23 - 127 with F the fp32 bits of float(r) (its exponent plus
+// mantissa fraction, since log2(1 + f) >= f on [0, 1]); on average the bound
+// sits within 0.46 of the noise, and the fixed recipe stays below it.  A token is skipped only when
 // z / T plus that bound plus a margin for every rounding involved (2^-17
 // relative, 2^-12 absolute) is still below y*: then a strictly larger value
 // exists and the token cannot be the draw.  Before the generator runs, the
@@ -367,7 +367,8 @@ struct SampleState {
 // One group of four tokens of one lane.  FIRST (the wave's first full
 // group, no running best yet): the wave first takes the largest lower bound
 // on z / T + g over its 256 tokens as y*, from the integer alone:
-// g >= (min(L, 23) - 1) ln 2 for u >= 1/2 (since -ln u <= 2 (1 - u) there)
+// g >= (min(L, 23) - 1) ln 2 for u >= 1/2, L the leading bits of the
+// generator word equal to its top bit (since -ln u <= 2 (1 - u) there)
 // and g >= -2.82 for u < 1/2, less the same rounding allowance; every value
 // is at most some token's exact z / T + g, and the token reaching it is never
 // skipped, so the exact draw is kept.
@@ -390,16 +391,14 @@ __device__ __forceinline__ void sample_group(const AcceptParams& p, const float 
   }
   unsigned c[4] = {(unsigned)e4 >> 2, node, seq, rnd};
   philox4x32_10(c, p.seed_lo, p.seed_hi);
-  int lead[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) lead[j] = min(__builtin_clrsb((int)c[j]) + 1, 23);  // leading bits equal to the top bit
   if (FIRST) {
     int lo_key = (int)0x80000000;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
+      const int lead = min(__builtin_clrsb((int)c[j]) + 1, 23);  // leading bits equal to the top bit
       const float zt = z[j] * inv_t;
       const float zt_lo = zt * (zt >= 0.f ? 1.0f - 0x1p-17f : 1.0f + 0x1p-17f);
-      const float g_lo = (int)c[j] < 0 ? (float)(lead[j] - 1) * kLn2 : -2.82f;
+      const float g_lo = (int)c[j] < 0 ? (float)(lead - 1) * kLn2 : -2.82f;
       lo_key = max(lo_key, float_order(__builtin_bit_cast(int, zt_lo + g_lo - 0x1p-12f)));
     }
     wbest = __builtin_bit_cast(float, float_order(wave_max_key(lo_key)));
@@ -409,7 +408,12 @@ __device__ __forceinline__ void sample_group(const AcceptParams& p, const float 
   for (int j = 0; j < 4; ++j) {
     if (TAIL && e4 + j >= c1) break;
     const float zt = z[j] * inv_t;
-    const float bound = fmaf((float)lead[j], kLn2, fmaf(fabsf(zt), 0x1p-17f, zt) + (slack + kLn2));
+    // upper bound on the noise: g <= -ln(1 - u) <= (23 - log2 r) ln 2 with
+    // r = 2^23 - 1 - k, log2 r bounded below by the fp32 bits of float(r)
+    // read as exponent plus mantissa fraction (r = 0: 150 ln 2)
+    const unsigned r = 0x7FFFFFu - (c[j] >> 9);
+    const float lg2r = (float)__builtin_bit_cast(unsigned, (float)r) * 0x1p-23f - 127.f;
+    const float bound = fmaf(23.f - lg2r, kLn2, fmaf(fabsf(zt), 0x1p-17f, zt) + slack);
     if (!(bound < wbest)) {
       const float y = gumbel_logit(z[j], p.temperature, c[j]);
       const int k = order_key(__builtin_bit_cast(unsigned, y));

@@ -178,6 +178,16 @@ def test_gumbel_bound_by_leading_zeros():
     top1 = top == 1
     lower = np.where(top1, (np.minimum(lead, 23) - 1) * np.log(2.0), -2.82)
     assert np.all(g >= lower)
+    # a tighter integer-only form: with r = 2^23 - 1 - k and F the fp32 bits of
+    # float(r), F 2^-23 - 127 <= log2 r (exponent plus mantissa fraction, since
+    # log2(1 + f) >= f on [0, 1]), so g <= -ln(1 - u) <= (23 - (F 2^-23 - 127)) ln 2;
+    # r = 0 gives 150 ln 2, far above the largest noise.  Computed in fp32 as a
+    # sampler would (the scaling by 2^-23 is exact).
+    r32 = (np.uint32(0x7FFFFF) - k).astype(np.uint32)
+    lg = r32.astype(np.float32).view(np.uint32).astype(np.float32) * np.float32(2.0 ** -23) - np.float32(127.0)
+    tight = (np.float32(23.0) - lg).astype(np.float64) * np.log(2.0)
+    assert np.all(g <= tight + 2.0 ** -16)
+    assert np.mean(tight - g) < 0.5 < np.mean(bound - g)   # tighter on average than the leading-bit form
     # the same bound read as clz(r) - 8 for u >= 1/2
     r = (np.uint32(0x7FFFFF) - k).astype(np.int64)
     hi = top == 1
