@@ -255,3 +255,22 @@ def test_device_round_counter_gives_fresh_noise_on_graph_replays():
     # without a counter the same by-value round gives the same draws
     a = _run(logits, par, tok, 1.0, seed, base + 3)
     assert np.array_equal(a["draws"], seen[2])
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_root_only_trees(dtype):
+    """n_nodes = 1 (the tree is just the root): nothing is accepted and the
+    next root is the root row's draw (sampling) or argmax (greedy)."""
+    g = torch.Generator().manual_seed(31)
+    logits = torch.randn((3, 1, 5000), generator=g).to(dtype)
+    par = torch.full((3, 1), -1, dtype=torch.int32)
+    tok = torch.tensor([[7], [8], [9]], dtype=torch.int32)
+    got = _run(logits, par, tok, 0.8, 99, 5, path_stride=1)
+    _check(got, logits, par, tok, 0.8, 99, 5, path_stride=1)
+    assert got["accept_len"].tolist() == [0, 0, 0]
+    assert got["next_root"].tolist() == got["draws"][:, 0].tolist()
+    greedy = G.glance_greedy_accept(logits.cuda(), par.cuda(), tok.cuda(), path_stride=1)
+    torch.cuda.synchronize()
+    assert greedy["accept_len"].cpu().tolist() == [0, 0, 0]
+    assert greedy["next_root"].cpu().tolist() == logits.float().argmax(-1)[:, 0].tolist()
+    assert greedy["accept_path"].cpu().tolist() == [[0], [0], [0]]
