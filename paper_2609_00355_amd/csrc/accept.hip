@@ -366,12 +366,12 @@ struct SampleState {
 
 // One group of four tokens of one lane.  FIRST (the wave's first full
 // group, no running best yet): the wave first takes the largest lower bound
-// on z / T + g over its 256 tokens as y*, from the integer alone:
-// g >= (min(L, 23) - 1) ln 2 for u >= 1/2, L the leading bits of the
-// generator word equal to its top bit (since -ln u <= 2 (1 - u) there)
-// and g >= -2.82 for u < 1/2, less the same rounding allowance; every value
-// is at most some token's exact z / T + g, and the token reaching it is never
-// skipped, so the exact draw is kept.
+// on z / T + g over its 256 tokens as y*, from the integer alone: for
+// u >= 1/2, -ln u <= (1 - u) / u gives g >= -ln(1 - u) - 2 (1 - u), bounded
+// below through the fp32 bits of float(r + 1) (within about 0.05 of the
+// noise in its upper tail); g >= -2.82 for u < 1/2; less the same rounding
+// allowance.  Every value is at most some token's exact z / T + g, and the
+// token reaching it is never skipped, so the exact draw is kept.
 template <bool TAIL, bool FIRST>
 __device__ __forceinline__ void sample_group(const AcceptParams& p, const float (&z)[4], int e4, int c1,
                                              unsigned node, unsigned seq, unsigned rnd, float& wbest,
@@ -395,10 +395,12 @@ __device__ __forceinline__ void sample_group(const AcceptParams& p, const float 
     int lo_key = (int)0x80000000;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int lead = min(__builtin_clrsb((int)c[j]) + 1, 23);  // leading bits equal to the top bit
       const float zt = z[j] * inv_t;
       const float zt_lo = zt * (zt >= 0.f ? 1.0f - 0x1p-17f : 1.0f + 0x1p-17f);
-      const float g_lo = (int)c[j] < 0 ? (float)(lead - 1) * kLn2 : -2.82f;
+      // r + 1 = 2^23 - k; log2(r + 1) <= F 2^-23 - 127 + 0.0861 for F the bits of float(r + 1)
+      const float r1 = (float)(0x800000u - (c[j] >> 9));
+      const float lg1 = (float)__builtin_bit_cast(unsigned, r1) * 0x1p-23f - 127.f;
+      const float g_lo = (int)c[j] < 0 ? (22.9138f - lg1) * kLn2 - 2.f * (r1 * 0x1p-23f) : -2.82f;
       lo_key = max(lo_key, float_order(__builtin_bit_cast(int, zt_lo + g_lo - 0x1p-12f)));
     }
     wbest = __builtin_bit_cast(float, float_order(wave_max_key(lo_key)));

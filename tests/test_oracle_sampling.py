@@ -188,6 +188,15 @@ def test_gumbel_bound_by_leading_zeros():
     tight = (np.float32(23.0) - lg).astype(np.float64) * np.log(2.0)
     assert np.all(g <= tight + 2.0 ** -16)
     assert np.mean(tight - g) < 0.5 < np.mean(bound - g)   # tighter on average than the leading-bit form
+    # a tighter lower bound for u >= 1/2: -ln u <= (1 - u) / u gives
+    # g >= -ln(1 - u) - 2 (1 - u), and with F the fp32 bits of float(r + 1),
+    # log2(r + 1) <= F 2^-23 - 127 + 0.0861 (the largest gap between
+    # log2(1 + f) and f), so g >= (23 - 0.0862 - (F 2^-23 - 127)) ln 2 - 2 (r + 1) 2^-23
+    r1 = (np.uint32(0x800000) - k).astype(np.uint32)
+    lg1 = r1.astype(np.float32).view(np.uint32).astype(np.float32) * np.float32(2.0 ** -23) - np.float32(127.0)
+    lo_tight = (np.float32(22.9138) - lg1) * np.float32(0.6931472) - \
+        np.float32(2.0) * (r1.astype(np.float32) * np.float32(2.0 ** -23))
+    assert np.all(g[top1] >= lo_tight[top1].astype(np.float64) + 2.0 ** -16)
     # the same bound read as clz(r) - 8 for u >= 1/2
     r = (np.uint32(0x7FFFFF) - k).astype(np.int64)
     hi = top == 1
