@@ -107,7 +107,7 @@ def load_traffic(kernel_key, src):
 
 COPY_BYTES = 256 << 20
 COPY_KERNEL = "neg_kernel"  # the calibration copy: out = -in over COPY_BYTES of fp32
-KERNEL_KEYS = {"draft": "attn_bf16_partial<128, false", "verify": "attn_bf16_partial<128, true",
+KERNEL_KEYS = {"draft": "attn_bf16<128, false", "verify": "attn_bf16<128, true",
                "accept": "argmax_partial<true, true>", "tree_stats": "tree_stats<true>",
                "tree_cands": "tree_cands<true>", "tree_rank": "tree_rank<true>", "tree_enum": "tree_enum",
                "sample": "sample_partial<true, true>"}
@@ -474,10 +474,10 @@ def main():
     f_verify = attn_flops(w, ctx, w.n_tree, vis_tree)
     logit_bytes = w.batch * w.n_tree * w.vocab * 2
     per_kernel = {
-        "draft": {"us": round(k_us["draft"], 2), "kernel": "attn_bf16_partial<128,false>",
+        "draft": {"us": round(k_us["draft"], 2), "kernel": "attn_bf16<128,false>",
                   "gbps": round((kvb + qo_draft) / k_us["draft"] / 1e3, 1),
                   "tflops": round(f_draft / k_us["draft"] / 1e6, 1)},
-        "verify": {"us": round(k_us["verify"], 2), "kernel": "attn_bf16_partial<128,true>",
+        "verify": {"us": round(k_us["verify"], 2), "kernel": "attn_bf16<128,true>",
                    "gbps": round((kvb + qo_verify) / k_us["verify"] / 1e3, 1),
                    "tflops": round(f_verify / k_us["verify"] / 1e6, 1)},
         "accept": {"us": round(k_us["accept"], 2), "kernel": "argmax_partial<true,true>",

@@ -86,9 +86,6 @@ typedef enum { GLANCE_F32 = 0, GLANCE_BF16 = 1 } glance_dtype;
  *   ctx_capacity  token stride of the context cache (>= every ctx_len), >= 0
  *   sm_scale      softmax scale; <= 0 selects 1/sqrt(head_dim)
  *   dtype         dtype of Q, K, V and O
- *   split_keys    context keys per split-KV work item; 0 lets the library
- *                 choose.  Otherwise a multiple of 64.  Results agree with any
- *                 other choice within rounding.
  */
 typedef struct {
   int32_t batch;
@@ -99,7 +96,6 @@ typedef struct {
   int32_t ctx_capacity;
   float sm_scale;
   glance_dtype dtype;
-  int32_t split_keys;
 } glance_attn_shape;
 
 /*
@@ -120,7 +116,7 @@ typedef struct {
  *   out       device [batch][n_new][Hq][D]              dtype
  *   lse       device [batch][n_new][Hq] float32 natural-log sum-exp of the
  *             scaled scores, or NULL
- *   workspace device, >= glance_attn_workspace_size(s) bytes, 256-byte aligned
+ *   workspace device, >= glance_attn_workspace_size(s, 0) bytes, 256-byte aligned
  */
 glance_status glance_block_draft_attn(const glance_attn_shape* s, const void* q, const void* k_ctx,
                                       const void* v_ctx, const void* k_new, const void* v_new,
@@ -305,9 +301,11 @@ glance_status glance_build_tree(int32_t batch, int32_t horizon, int32_t vocab, i
 /* Workspace bytes glance_build_tree needs (0 if the sizes are invalid). Host only. */
 size_t glance_tree_workspace_size(int32_t batch, int32_t horizon, int32_t vocab, int32_t budget);
 
-/* Workspace bytes an attention call with shape *s needs (0 if *s is invalid).
- * The same size serves the draft and the verify entry point. Host only. */
-size_t glance_attn_workspace_size(const glance_attn_shape* s);
+/* Workspace bytes an attention call with shape *s needs (0 if *s is invalid):
+ * is_verify = 0 for glance_block_draft_attn, 1 for glance_tree_verify_attn.
+ * The two sizes are equal in this build, so one workspace serves both calls
+ * of a shape.  The size depends on the shape only. Host only. */
+size_t glance_attn_workspace_size(const glance_attn_shape* s, int32_t is_verify);
 
 /* Workspace bytes glance_greedy_accept needs (0 if the sizes are invalid). Host only. */
 size_t glance_accept_workspace_size(int32_t batch, int32_t n_nodes, int32_t vocab);
@@ -331,9 +329,9 @@ const char* glance_last_error(void);
 /*
  * Profiling hook.  When both events are non-NULL, the next attention, accept,
  * commit or tree-builder call on this thread records `start` on its stream
- * right before its main kernel (the split-KV attention kernel, the vocabulary
- * argmax kernel, the commit kernel, or all passes of the tree builder) and
- * `stop` right after it, then forgets the pair.  Arguments are hipEvent_t handles created by
+ * right before its main kernel (the attention and its merge pass, the
+ * vocabulary argmax kernel, the commit kernel, or all passes of the tree
+ * builder) and `stop` right after it, then forgets the pair.  Arguments are hipEvent_t handles created by
  * the caller.  Pass NULLs to clear.
  */
 glance_status glance_set_kernel_events(void* start_event, void* stop_event);

@@ -43,7 +43,7 @@ class AttnShape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_new", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("ctx_capacity", ctypes.c_int32), ("sm_scale", ctypes.c_float),
-                ("dtype", ctypes.c_int), ("split_keys", ctypes.c_int32)]
+                ("dtype", ctypes.c_int)]
 
 
 _lib = None
@@ -66,7 +66,7 @@ _SIGS = {
     "glance_tree_workspace_size": (_SZ, [_I32, _I32, _I32, _I32]),
     "glance_commit_path": (ctypes.c_int, [_I32, _I32, _I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _I32, _P,
                                           _P, _P, _P]),
-    "glance_attn_workspace_size": (_SZ, [ctypes.POINTER(AttnShape)]),
+    "glance_attn_workspace_size": (_SZ, [ctypes.POINTER(AttnShape), _I32]),
     "glance_accept_workspace_size": (_SZ, [_I32, _I32, _I32]),
     "glance_validate_tree": (ctypes.c_int, [_I32, _P, _P, _I32]),
     "glance_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -118,14 +118,13 @@ def glance_validate_tree(parents, tokens=None, max_depth=-1):
     return st == GLANCE_OK, ("" if st == GLANCE_OK else glance_last_error())
 
 
-def attn_shape(batch, n_new, n_q_heads, n_kv_heads, head_dim, ctx_capacity, dtype, sm_scale=0.0,
-               split_keys=0):
+def attn_shape(batch, n_new, n_q_heads, n_kv_heads, head_dim, ctx_capacity, dtype, sm_scale=0.0):
     return AttnShape(int(batch), int(n_new), int(n_q_heads), int(n_kv_heads), int(head_dim),
-                     int(ctx_capacity), float(sm_scale), int(dtype), int(split_keys))
+                     int(ctx_capacity), float(sm_scale), int(dtype))
 
 
-def glance_attn_workspace_size(shape):
-    return int(lib().glance_attn_workspace_size(ctypes.byref(shape)))
+def glance_attn_workspace_size(shape, is_verify=0):
+    return int(lib().glance_attn_workspace_size(ctypes.byref(shape), int(is_verify)))
 
 
 def glance_accept_workspace_size(batch, n_nodes, vocab):
@@ -182,16 +181,31 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _workspace(nbytes, device, workspace):
+def _workspace(nbytes, device, workspace, stream=None):
+    """The caller's workspace, or a new one allocated on the stream the call
+    runs on, so that the caching allocator does not hand it to other work
+    while the call's kernels still use it."""
     torch = _torch()
     if workspace is not None:
         return workspace
     # 256-byte aligned by the caching allocator
+    if stream is not None and stream != torch.cuda.current_stream(device):
+        with torch.cuda.stream(stream):
+            return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
 
 
+def _new_output(make, like, stream, **kw):
+    """A new output tensor, allocated on the stream the call runs on."""
+    torch = _torch()
+    if stream is not None and stream != torch.cuda.current_stream():
+        with torch.cuda.stream(stream):
+            return make(like, **kw)
+    return make(like, **kw)
+
+
 def _attn(tree, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, workspace, sm_scale,
-          split_keys, stream, want_lse):
+          stream, want_lse):
     torch = _torch()
     _dev(q, "q", ndim=4)
     dt = q.dtype
@@ -217,19 +231,19 @@ def _attn(tree, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, work
         _dev(parents, "parents", torch.int32, 2)
         if tuple(parents.shape) != (batch, n):
             raise ValueError("parents must be [batch][n]")
-    shape = attn_shape(batch, n, hq, hkv, d, cap, code, sm_scale, split_keys)
+    shape = attn_shape(batch, n, hq, hkv, d, cap, code, sm_scale)
     if out is None:
-        out = torch.empty_like(q)
+        out = _new_output(torch.empty_like, q, stream)
     else:
         _dev(out, "out", dt, 4)
     if lse is None and want_lse:
-        lse = torch.empty((batch, n, hq), dtype=torch.float32, device=q.device)
+        lse = _new_output(torch.empty, (batch, n, hq), stream, dtype=torch.float32, device=q.device)
     elif lse is not None:
         _dev(lse, "lse", torch.float32, 3)
-    need = glance_attn_workspace_size(shape)
+    need = glance_attn_workspace_size(shape, int(tree))
     if need == 0:
         raise GlanceError(GLANCE_ERR_INVALID_ARG, glance_last_error())
-    ws = _workspace(need, q.device, workspace)
+    ws = _workspace(need, q.device, workspace, stream)
     common = [ctypes.byref(shape), _ptr(q), _ptr(k_ctx), _ptr(v_ctx), _ptr(k_new), _ptr(v_new),
               _ptr(ctx_lens)]
     if tree:
@@ -243,17 +257,17 @@ def _attn(tree, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, work
 
 
 def glance_block_draft_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, out=None, lse=None, workspace=None,
-                            sm_scale=0.0, split_keys=0, stream=None, want_lse=True):
+                            sm_scale=0.0, stream=None, want_lse=True):
     """Block-draft attention (bidirectional block over the cached context).  Returns (out, lse)."""
     return _attn(False, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, None, out, lse, workspace, sm_scale,
-                 split_keys, stream, want_lse)
+                 stream, want_lse)
 
 
 def glance_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out=None, lse=None,
-                            workspace=None, sm_scale=0.0, split_keys=0, stream=None, want_lse=True):
+                            workspace=None, sm_scale=0.0, stream=None, want_lse=True):
     """Ancestor-masked tree-verify attention.  Returns (out, lse)."""
     return _attn(True, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, workspace, sm_scale,
-                 split_keys, stream, want_lse)
+                 stream, want_lse)
 
 
 def glance_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None, workspace=None,
@@ -443,15 +457,15 @@ class PreparedCall:
 
 
 def _prepare_attn(tree, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, workspace, sm_scale,
-                  split_keys, stream):
+                  stream):
     batch, n, hq, d = q.shape
     hkv = k_new.shape[2]
     cap = 0 if (k_ctx is None or k_ctx.numel() == 0) else k_ctx.shape[2]
-    shape = attn_shape(batch, n, hq, hkv, d, cap, _dtype_code(q), sm_scale, split_keys)
-    ws = _workspace(glance_attn_workspace_size(shape), q.device, workspace)
+    shape = attn_shape(batch, n, hq, hkv, d, cap, _dtype_code(q), sm_scale)
+    ws = _workspace(glance_attn_workspace_size(shape, int(tree)), q.device, workspace, stream)
     # one checked call establishes outputs and validates everything; then freeze the arguments
     out, lse = _attn(tree, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, ws,
-                     sm_scale, split_keys, stream, lse is not None)
+                     sm_scale, stream, lse is not None)
     if cap == 0:
         k_ctx = v_ctx = None
     args = [ctypes.byref(shape), _ptr(q), _ptr(k_ctx), _ptr(v_ctx), _ptr(k_new), _ptr(v_new),
@@ -466,17 +480,17 @@ def _prepare_attn(tree, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, l
 
 
 def prepare_block_draft_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, out=None, lse=None, workspace=None,
-                             sm_scale=0.0, split_keys=0, stream=None):
+                             sm_scale=0.0, stream=None):
     """Returns (call, out, lse): call() re-runs the draft attention into out / lse."""
     return _prepare_attn(False, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, None, out, lse, workspace,
-                         sm_scale, split_keys, stream)
+                         sm_scale, stream)
 
 
 def prepare_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out=None, lse=None,
-                             workspace=None, sm_scale=0.0, split_keys=0, stream=None):
+                             workspace=None, sm_scale=0.0, stream=None):
     """Returns (call, out, lse): call() re-runs the tree-verify attention into out / lse."""
     return _prepare_attn(True, q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, out, lse, workspace,
-                         sm_scale, split_keys, stream)
+                         sm_scale, stream)
 
 
 def prepare_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None, workspace=None,

@@ -1,92 +1,101 @@
 // Split-KV attention for the block draft and the ancestor-masked tree verify,
 // bf16 in / fp32 accumulate, on gfx950 matrix cores.
 //
-// One workgroup owns one (sequence b, KV head g, context split s, row group).
-// Its rows are the flattened (new row, query head of the group) pairs, so the
-// K/V tile staged in LDS is shared by every query head of the GQA group and
-// by every block/tree row: the context is read from HBM once per split.
+// Work items.  The rows of one (sequence b, KV head g) problem are the
+// flattened (new row, query head of the GQA group) pairs, so one K/V tile in
+// LDS serves every query head of the group and every block or tree row.  The
+// rows form row groups of up to seven 32-row tiles; the keys of a sequence
+// (its context tiles of 64 keys, then one tile holding the block or tree keys)
+// are cut into pieces.  A workgroup owns one (piece, row group).  The pieces
+// are planned on the device from ctx_lens, the same way by every workgroup:
+// each sequence of len_b tiles gets n_b = ceil(len_b / T) pieces of nearly
+// equal size, with T the smallest size for which all pieces fit the launched
+// slots; so a ragged batch gets pieces of equal cost rather than equal key
+// ranges, and no slot is spent on a sequence's padding.
 //
-// K/V tiles of 64 keys stream from HBM straight into LDS (global_load_lds,
-// 16 bytes per lane, no register staging) through a ring of kStages buffers,
-// so several tiles are in flight per workgroup while the current one is
-// consumed.  Rows of the tile are stored unpadded with the 16-byte chunks of
-// key k permuted by an XOR with swz(k), which keeps both the K-operand reads
-// and the transposed V reads free of bank conflicts.  The loads are issued
-// from inline assembly and waited for explicitly (s_waitcnt vmcnt), because
-// the compiler, seeing a load into LDS in flight, would otherwise wait for
-// all of them before every LDS read and drain the ring.
+// Waves.  Waves 0 .. tiles-1 compute one 32-row tile each.  All 8 waves
+// stream K/V tiles from HBM straight into LDS (global_load_lds, 16 bytes per
+// lane, no register staging), each its share of every tile, through rings
+// of four K stages and four V stages; one LDS barrier per tile orders the
+// loads and the reads (the ring's rule is stated at ring_wait).
 //
-// Per tile each wave computes, for each of its 16-row tiles,
-//   S^T[key][row] = K[key][:] . Q[row][:]        (v_mfma_f32_16x16x32_bf16, A = K, B = Q^T)
-//   online softmax over the keys of each row    (exp2 with the scale folded in)
-//   O^T[d][row]  += V^T[d][key] . P^T[key][row] (A = V^T via ds_read_b64_tr_b16, B = P^T)
-// S^T is computed with the key order permuted inside each 32-key group so
-// that the MFMA result layout (lane l holds rows l%16, key slots 4*(l/16)+i)
-// is directly the B operand of the P.V product (lane l needs 8 consecutive
-// key slots 8*(l/16)..+7): no shuffle between the two contractions.
+// Per tile a computing wave runs, for its 32 rows and the tile's 64 keys,
+//   S^T[key][row] = K[key][:] . Q[row][:]           (v_mfma_f32_32x32x16_bf16, A = K, B = Q^T)
+//   P = exp2(S c - m c)                              (online softmax, lazily rescaled)
+//   O^T[d][row] += V^T[d][key] . P^T[key][row]     (A = V^T by ds_read_b64_tr_b16, B = P^T)
+// as a matrix phase (Q.K^T of tile t with P.V of tile t-1) and a vector phase
+// (the softmax of tile t); the two waves that share a SIMD overlap one's
+// matrix phase with the other's vector phase.  The
+// MFMA result layout of S^T (lane l: row l%32, keys 8j + 4(l/32) + i) is used
+// directly as the B operand of P.V by ordering the keys of each 16-key k-step
+// accordingly (no shuffles), and the row of a lane never changes, so the
+// running max and sum are per lane (lanes l and l+32 share a row).
 //
-// The new keys (block or tree rows) are one extra tile processed by the last
-// split of each sequence; for the tree, node i sees key j iff bit j of its
-// ancestor word is set (Def. 1's packed verification).  Each split writes its
-// unnormalised output and (max, sum) to the workspace; attn_merge.hip
-// combines the splits.
+// Merge.  A piece that is its sequence's only one writes the output and LSE.
+// Otherwise each piece writes its unnormalised output (in the MFMA register
+// layout, one float4 per lane per store) and (max, sum) per row to the
+// workspace, and attn_merge.hip combines the pieces in a second, fully
+// parallel pass; the first piece of each sequence records the sequence's
+// piece count and first slot for it.
 #include "glance_internal.h"
-
-#include <type_traits>
 
 namespace glance {
 namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) char lds_char;
 
 constexpr float kNegInf = -__builtin_inff();
-constexpr int kStages = 4;     // LDS ring depth: tiles in flight per workgroup
-constexpr float kSlack = 8.f;  // lazy-rescale threshold (exp2 units)
+constexpr int kStages = 4;          // LDS ring depth (tiles)
+constexpr float kSumLimit = 256.f;  // per-lane probability sum that forces a rescale
+constexpr float kLn2 = 0.6931471805599453f;
+#ifndef GLANCE_AHEAD
+#define GLANCE_AHEAD 2
+#endif
+#ifndef GLANCE_XPRIO
+#define GLANCE_XPRIO 0
+#endif
+constexpr int kOperandsAhead = GLANCE_AHEAD;  // LDS operand reads issued ahead of their MFMA
 
+// Key-tile geometry for head dimension D (bf16 rows, unpadded).
 template <int D>
-struct Geom {
-  static constexpr int kRowBytes = D * 2;                    // one key row, unpadded
-  static constexpr int kChunks = D / 8;                      // 16-byte chunks per row
-  static constexpr int kKeysPerInst = 64 / kChunks;          // rows filled by one wave load
-  static constexpr int kTileBytes = kKeyTile * kRowBytes;    // one K (or V) tile
-  static constexpr int kInstPerWave = kKeyTile / (kKeysPerInst * kBf16Waves);
+struct Geo {
+  static constexpr int RB = 2 * D;      // bytes per key row
+  static constexpr int CH = D / 8;      // 16-byte chunks per row
+  static constexpr int TB = 64 * RB;    // bytes of one K (or V) tile
+  static constexpr int KS = D / 16;     // k-steps of Q.K^T (16 dims each)
+  static constexpr int DB = D / 32;     // 32-dim blocks of P.V
+  static constexpr int RPL = 1024 / RB; // key rows per 1 KB load instruction
+  static constexpr int NB = 64 / RPL;   // load instructions per K (or V) tile
+  static constexpr int OV = D / 2;      // fp32 output values per lane (32 rows x D / 64)
 };
 
-// Chunk permutation of key row k (XOR, so a bijection on the chunks of a row).
-// Lanes 0-7 of a K-operand read touch rows {0-3, 8-11} (+16 for lanes 8-15) at
-// one chunk; lanes of a transposed V read touch 4 consecutive rows at two
-// neighbouring chunks.  Both land on distinct 16-byte bank groups.
+// Chunk c of key row r sits at chunk c ^ swz(r) of the row's LDS slot.  The
+// LDS serves 64 banks of 4 bytes; a K-operand read (16 bytes per lane) covers
+// 16 consecutive rows at one chunk per 16 lanes, and a transposed V read
+// covers 4 consecutive rows x 2 chunks per 16 lanes.  swz is a bijection on
+// the 16-byte bank groups over every aligned run of 16 rows (bits 0-3), and
+// over every aligned run of 4 rows both bits 1-2 and bits 2-3 run through all
+// four values, so both reads are free of bank conflicts (measured against
+// simpler permutations).  For D = 64 (8 chunks per row) only bits 0-2 apply.
 template <int D>
-__device__ __forceinline__ int swz(int k) {
-  if (D >= 128) return ((k & 3) << 1) | (((k >> 3) & 1) << 3) | ((k >> 4) & 1);
-  return ((k & 3) << 1) | ((k >> 3) & 1);
+__device__ __forceinline__ int swz(int r) {
+  const int t = 8 * ((r >> 1) & 1) + 4 * (r & 1) + 2 * (((r >> 1) ^ r) & 1) + ((r >> 2) & 1);
+  const int s = t ^ (((r >> 3) & 1) << 1);
+  return D >= 128 ? s : (s & 7);
 }
 
 // One 16-byte-per-lane load from global memory into LDS: lane i writes LDS
-// bytes [lds_base + 16 i, +16).  M0 carries the wave-uniform LDS base; it is
-// saved and restored around the load (the compiler owns M0), and one wait
-// state separates the M0 write from the load that reads it.
-__device__ __forceinline__ void dma16(const void* gptr, unsigned lds_base) {
-  unsigned saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %2, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(lds_base), "v"(gptr)
-      : "memory");
-}
-
-// The same load with a wave-uniform 64-bit base in SGPRs and a 32-bit
-// per-lane byte offset: no per-lane address arithmetic at issue.
-__device__ __forceinline__ void dma16s(const void* sbase, unsigned voff, unsigned lds_base) {
+// bytes [lds + 16 i, +16) with data from sbase + voff.  M0 carries the LDS
+// address; it is saved and restored around the load (the compiler owns M0).
+__device__ __forceinline__ void dma16(const void* sbase, unsigned voff, unsigned lds) {
   unsigned saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
@@ -95,538 +104,538 @@ __device__ __forceinline__ void dma16s(const void* sbase, unsigned voff, unsigne
       "global_load_lds_dwordx4 %2, %3\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "s"(lds_base), "v"(voff), "s"(sbase)
+      : "s"(lds), "v"(voff), "s"(sbase)
       : "memory");
 }
 
-// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
+// s_waitcnt vmcnt(N), other counters left alone (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
 }
 
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+// Barrier that orders LDS only: this wave's LDS operations finish, then
+// s_barrier.  (__syncthreads() also waits for every outstanding global load,
+// which would drain the ring.)
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// Workgroup barrier for the DMA ring.  __syncthreads() carries a release fence,
-// which would make every wave wait for all of its outstanding global->LDS
-// loads (vmcnt(0)) and drain the ring.  Here each wave has already waited for
-// the loads of the tile it is about to read (wait_vmcnt), so the barrier only
-// has to order LDS: finish this wave's own LDS operations, then s_barrier.  The
-// "memory" clobber keeps the compiler from moving LDS accesses across it.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+__device__ __forceinline__ int wave_max(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off));
+  return v;
 }
 
-template <int D, bool TREE, int TPW>
-__global__ __launch_bounds__(kBf16Waves * 64) void attn_bf16_partial(AttnParams p) {
-  using G_ = Geom<D>;
-  constexpr int KS = D / 32;  // k-steps of Q.K^T
-  constexpr int DT = D / 16;  // d-tiles of P.V
-  constexpr int RB = G_::kRowBytes;
-  constexpr int CH = G_::kChunks;
-  constexpr int IPW = G_::kInstPerWave;
-  constexpr int LOADS_PER_TILE = 2 * IPW;  // K and V load instructions per wave per tile
-  constexpr int kAhead = kStages - 1;  // tiles streaming behind the current one
-  static_assert(IPW * G_::kKeysPerInst * kBf16Waves == kKeyTile, "tile load must divide evenly");
+__device__ __forceinline__ int clamp_ctx(int ctx, int cap) { return ctx < 0 ? 0 : (ctx > cap ? cap : ctx); }
+// tiles of a sequence: its context tiles, then the tile of new keys
+__device__ __forceinline__ int seq_tiles(int ctx) { return (ctx + 63) / 64 + 1; }
 
-  __shared__ __attribute__((aligned(1024))) char sRing[kStages][2][G_::kTileBytes];
+struct Piece {
+  int b;        // sequence
+  int first;    // piece slot of the sequence's first piece (within the KV head)
+  int count;    // pieces of the sequence
+  int index;    // this piece's index among them
+  int t_begin;  // first tile (of the sequence's tile list)
+  int n_tiles;  // tiles of the piece, >= 1
+  int ctx;      // context keys of the sequence
+};
+
+// The piece plan (identical in every wave of every workgroup): T is the
+// smallest piece size, at least min_tiles, with sum_b ceil(len_b / T) <=
+// slots; piece slot ps then names piece ps - first_b of the sequence b with
+// first_b <= ps < first_b + n_b.  Returns false if the slot is unused.  The
+// lengths are read once (sequences lane + 64 k, k < kPlanCache, held in
+// registers; larger batches re-read the rest), since every memory round trip
+// here delays the first tile load.
+constexpr int kPlanCache = 4;
+__device__ bool find_piece(const AttnParams& p, int ps, int lane, Piece& out) {
+  int len_c[kPlanCache], ctx_c[kPlanCache];
+#pragma unroll
+  for (int k = 0; k < kPlanCache; ++k) {
+    const int b = lane + 64 * k;
+    ctx_c[k] = b < p.batch ? clamp_ctx(p.ctx_lens[b], p.cap) : 0;
+    len_c[k] = b < p.batch ? seq_tiles(ctx_c[k]) : 0;
+  }
+  auto len_of = [&](int k, int b) __attribute__((always_inline)) {
+    return k < kPlanCache ? len_c[k] : (b < p.batch ? seq_tiles(clamp_ctx(p.ctx_lens[b], p.cap)) : 0);
+  };
+  int total = 0, longest = 0;
+  for (int b0 = 0, k = 0; b0 < p.batch; b0 += 64, ++k) {
+    const int len = len_of(k, b0 + lane);
+    total += len;
+    longest = max(longest, len);
+  }
+  total = wave_sum(total);
+  longest = wave_max(longest);
+  const int slots = p.slots_per_g;
+  auto count = [&](int T) __attribute__((always_inline)) {
+    int cnt = 0;
+    for (int b0 = 0, k = 0; b0 < p.batch; b0 += 64, ++k) cnt += (len_of(k, b0 + lane) + T - 1) / T;
+    return wave_sum(cnt);
+  };
+  int lo = max(p.min_tiles, (total + slots - 1) / slots);
+  int hi = max(lo, longest);  // with T = longest every sequence is one piece; slots >= batch
+  if (count(lo) <= slots) hi = lo;  // exact for equal lengths
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (count(mid) <= slots) hi = mid;
+    else lo = mid + 1;
+  }
+  const int T = __builtin_amdgcn_readfirstlane(lo);
+  int base = 0;
+  for (int b0 = 0, k = 0; b0 < p.batch; b0 += 64, ++k) {
+    const int b = b0 + lane;
+    const int ctx = k < kPlanCache ? ctx_c[k] : (b < p.batch ? clamp_ctx(p.ctx_lens[b], p.cap) : 0);
+    const int len = b < p.batch ? seq_tiles(ctx) : 0;
+    const int nb = (len + T - 1) / T;
+    int incl = nb;  // inclusive prefix sum over the lanes
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(incl, off);
+      if (lane >= off) incl += v;
+    }
+    incl += base;
+    const int excl = incl - nb;
+    const unsigned long long hit = __ballot(b < p.batch && excl <= ps && ps < incl);
+    if (hit) {
+      const int src = __ffsll((long long)hit) - 1;
+      out.b = b0 + src;
+      out.first = __shfl(excl, src);
+      out.count = __shfl(nb, src);
+      out.ctx = __shfl(ctx, src);
+      const int slen = __shfl(len, src);
+      out.index = ps - out.first;
+      out.t_begin = out.index * slen / out.count;
+      out.n_tiles = (out.index + 1) * slen / out.count - out.t_begin;
+      out.b = __builtin_amdgcn_readfirstlane(out.b);
+      out.first = __builtin_amdgcn_readfirstlane(out.first);
+      out.count = __builtin_amdgcn_readfirstlane(out.count);
+      out.ctx = __builtin_amdgcn_readfirstlane(out.ctx);
+      out.index = __builtin_amdgcn_readfirstlane(out.index);
+      out.t_begin = __builtin_amdgcn_readfirstlane(out.t_begin);
+      out.n_tiles = __builtin_amdgcn_readfirstlane(out.n_tiles);
+      return true;
+    }
+    base = __shfl(incl, 63);
+  }
+  return false;
+}
+
+template <int D, bool TREE>
+__global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
+  using G_ = Geo<D>;
+  constexpr int RB = G_::RB, CH = G_::CH, TB = G_::TB, KS = G_::KS, DB = G_::DB;
+  constexpr int RPL = G_::RPL, NB = G_::NB, OV = G_::OV;
+
+  __shared__ __attribute__((aligned(1024))) char sK[kStages * TB];
+  __shared__ __attribute__((aligned(1024))) char sV[kStages * TB];
   __shared__ unsigned long long sAnc[64];
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches
-  const int lg = lane >> 4;   // lane group 0..3
-  const int lr = lane & 15;   // row within a 16-row tile
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
-  // ---- work item.  Blocks 8*(row_groups*j + r) + x form group 8*j + x, row
-  // group r: the row groups sharing one KV split sit on the same XCD (block
-  // index mod 8), so their repeated K/V reads hit that XCD's L2.
+  // ---- work item.  Blocks 8 (rg j + r) + x hold slot 8 j + x, row group r:
+  // the row groups of one piece sit on one XCD (block index mod 8), so their
+  // repeated K/V reads hit that XCD's L2.
   const int L = blockIdx.x;
-  const int xcd = L & 7;
   const int q8 = L >> 3;
-  const int rg = q8 % p.row_groups;
-  const int grp = (q8 / p.row_groups) * 8 + xcd;
-  if (grp >= p.nsplit * p.batch * p.hkv) return;
-  const int g = grp % p.hkv;
-  const int bs = grp / p.hkv;
-  const int b = bs % p.batch;
-  const int s = bs / p.batch;
+  const int rgi = q8 % p.row_groups;
+  const int slot = (q8 / p.row_groups) * 8 + (L & 7);
+  if (slot >= p.slots_per_g * p.hkv) return;
+  const int g = slot / p.slots_per_g;
+  Piece pc;
+  if (!find_piece(p, slot - g * p.slots_per_g, lane, pc)) return;
+  const int b = pc.b;
+  const int ctx = pc.ctx;
+  const int ct = (ctx + 63) / 64;  // context tiles; tile ct holds the new keys
+  const int n_tiles = pc.n_tiles;
+  const int tb = pc.t_begin;
+  const bool has_new = tb + n_tiles - 1 == ct;
+  const bool split = pc.count > 1;
+  if (pc.index == 0 && g == 0 && rgi == 0 && threadIdx.x == 0)
+    p.plan[b] = make_int2(pc.count, pc.first);  // for the merge pass
 
-  int ctx = p.ctx_lens[b];
-  ctx = ctx < 0 ? 0 : (ctx > p.cap ? p.cap : ctx);
-  const int nsb = ctx > 0 ? (ctx + p.split_keys - 1) / p.split_keys : 1;
-  if (s >= nsb) return;  // empty split of a shorter sequence
-  const int k_begin = s * p.split_keys;
-  const int k_end = min(ctx, k_begin + p.split_keys);
-  const bool has_new = (s == nsb - 1);
-  const int n_ctx_tiles = k_end > k_begin ? (k_end - k_begin + kKeyTile - 1) / kKeyTile : 0;
-  const int n_tiles = n_ctx_tiles + (has_new ? 1 : 0);
-  // Full context tiles come first; the ragged last context tile and the
-  // new-key tile (if any) need the mask.
-  const int n_full = (k_end - k_begin) / kKeyTile;
-
-  const __bf16* q = static_cast<const __bf16*>(p.q);
+  // =========================== K/V streaming (all waves) ===========================
   const char* kc = static_cast<const char*>(p.k_ctx);
   const char* vc = static_cast<const char*>(p.v_ctx);
   const char* kn = static_cast<const char*>(p.k_new);
   const char* vn = static_cast<const char*>(p.v_new);
-
-  // ---- the loads of tile t into ring stage st.  Wave w fills rows
-  // [8w, 8w+8); lane i of a load writes LDS row base + i/CH, chunk slot i%CH,
-  // which holds global chunk slot ^ swz(row).  Rows past the valid keys re-read
-  // the last valid row: their scores are masked, so P = 0 and V is finite.
-  // Lane offsets of the wave's shares within a full context tile (all 64 rows
-  // valid, row stride RB), computed once; other tiles compute theirs at issue.
-  unsigned full_off[LOADS_PER_TILE / 2];
+  constexpr int SH = NB / 8;  // load instructions per wave per K (or V) tile
+  // Load r of a tile fills LDS rows r RPL .. r RPL + RPL - 1; lane i writes
+  // row r RPL + i / CH, chunk slot i % CH, which holds the row's chunk
+  // slot ^ swz(row).  This wave's loads are r = wave + 8 i.  Lane offsets
+  // within a full context tile (row stride RB) are computed once.
+  unsigned full_off[SH];
 #pragma unroll
-  for (int i = 0; i < LOADS_PER_TILE / 2; ++i) {
-    const int row = (wave * IPW + i) * G_::kKeysPerInst + lane / CH;
-    full_off[i] = (unsigned)(row * RB + ((lane % CH) ^ swz<D>(row)) * 16);
+  for (int i = 0; i < SH; ++i) {
+    const int row = (wave + 8 * i) * RPL + lane / CH;
+    full_off[i] = (unsigned)(row * RB + (((lane % CH) ^ swz<D>(row)) * 16));
   }
-  auto issue = [&](int t) __attribute__((always_inline)) {
-    // t is the same in every lane; say so, since the LDS base must sit in an SGPR
-    // (M0) and the compiler's uniformity analysis can lose track of it in loops
-    // whose bodies branch per lane.
-    t = __builtin_amdgcn_readfirstlane(t);
-    const unsigned lk = (unsigned)(size_t)(&sRing[t % kStages][0][0]);
-    const unsigned lv = (unsigned)(size_t)(&sRing[t % kStages][1][0]);
-    if (t < n_full) {
-      // one tile base for all of the wave's shares: SGPR base + lane offsets
-      const size_t off = (((size_t)b * p.hkv + g) * p.cap + k_begin + (size_t)t * kKeyTile) * RB;
+  auto issue = [&](int t, bool v_side) __attribute__((always_inline)) {
+    const char* gfull = v_side ? vc : kc;
+    const unsigned lds = (unsigned)(size_t)(v_side ? sV : sK) + (unsigned)(t % kStages) * TB;
+    const int j = tb + t;
+    if (j < ct && 64 * j + 64 <= ctx) {  // full context tile: SGPR base + fixed lane offsets
+      const size_t off = (((size_t)b * p.hkv + g) * p.cap + 64 * (size_t)j) * RB;
 #pragma unroll
-      for (int i = 0; i < LOADS_PER_TILE / 2; ++i) {
-        const unsigned lrow = (unsigned)((wave * IPW + i) * G_::kKeysPerInst * RB);
-        dma16s(kc + off, full_off[i], lk + lrow);
-        dma16s(vc + off, full_off[i], lv + lrow);
-      }
+      for (int i = 0; i < SH; ++i) dma16(gfull + off, full_off[i], lds + (wave + 8 * i) * 1024);
       return;
     }
-    const char* kb;
-    const char* vb;
-    size_t stride;
+    // ragged context tile or the new keys: rows past the valid ones re-read
+    // the last valid row (their scores are masked, so P = 0 and V is finite)
+    const char* base;
+    unsigned stride;
     int nvalid;
-    if (t < n_ctx_tiles) {
-      const int key0 = k_begin + t * kKeyTile;
-      nvalid = min(kKeyTile, k_end - key0);
-      const size_t off = (((size_t)b * p.hkv + g) * p.cap + key0) * RB;
-      kb = kc + off;
-      vb = vc + off;
+    if (j < ct) {
+      base = gfull + (((size_t)b * p.hkv + g) * p.cap + 64 * (size_t)j) * RB;
       stride = RB;
+      nvalid = ctx - 64 * j;
     } else {
+      base = (v_side ? vn : kn) + ((size_t)b * p.n * p.hkv + g) * RB;
+      stride = (unsigned)p.hkv * RB;
       nvalid = p.n;
-      const size_t off = ((size_t)b * p.n * p.hkv + g) * RB;
-      kb = kn + off;
-      vb = vn + off;
-      stride = (size_t)p.hkv * RB;
     }
-    // The lane's offsets are recomputed from a laundered lane id each time:
-    // hoisted out of the loop they would stay live across it and push the
-    // kernel into spilling (whose reloads wait for every tile load in flight).
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
 #pragma unroll
-    for (int i = 0; i < LOADS_PER_TILE / 2; ++i) {
-      const int row0 = (wave * IPW + i) * G_::kKeysPerInst;
-      const int row = row0 + ln / CH;
+    for (int i = 0; i < SH; ++i) {
+      const int row = (wave + 8 * i) * RPL + lane / CH;
       const int src = row < nvalid ? row : nvalid - 1;
-      const unsigned goff = (unsigned)src * (unsigned)stride + (unsigned)(((ln % CH) ^ swz<D>(row)) * 16);
-      dma16(kb + goff, lk + row0 * RB);
-      dma16(vb + goff, lv + row0 * RB);
+      dma16(base, (unsigned)src * stride + (unsigned)(((lane % CH) ^ swz<D>(row)) * 16), lds + (wave + 8 * i) * 1024);
     }
   };
-
-  // ---- ancestor words of the packed tree, anc[i] = {i} u anc[parent(i)], by
-  // pointer doubling in wave 0 (one load per node instead of a chain of
-  // dependent loads): after r rounds lane i holds the nodes on its root path
-  // from i up to (excluding) its 2^r-th ancestor up[i].
-  // The query and parent loads below are issued from inline assembly, like
-  // the tile loads, and waited for explicitly: the compiler counts only the
-  // loads it can see, so its own wait before their first use would be
-  // vmcnt(0) and would also wait for every tile load in flight.
-  unsigned long long anc_word = 0;
-  int up = -1;
-  int par_raw = -1;
-  const bool load_par = TREE && has_new && wave == 0 && lane < p.n;
-  if (load_par)
-    asm volatile("global_load_dword %0, %1, off" : "=v"(par_raw) : "v"(p.parents + (size_t)b * p.n + lane) : "memory");
-
-  // ---- this wave's query rows, held as MFMA B operands for the whole split.
-  const int n_row_tiles = (p.rows + 15) >> 4;
-  const int tile0 = rg * p.tiles_per_group + wave * TPW;
-  // Inactive tiles (past this row group or past the last row) compute on a
-  // zero query and are not written; a wave with none skips the arithmetic.
-  bool act[TPW];
-  bf16x8 qf[TPW][KS];
-  int node_of[TPW];
-  bool wave_active = false;
-#pragma unroll
-  for (int j = 0; j < TPW; ++j) {
-    act[j] = (wave * TPW + j < p.tiles_per_group) && (tile0 + j < n_row_tiles);
-    wave_active = wave_active || act[j];
-    const int row = (tile0 + j) * 16 + lr;
-    node_of[j] = p.n;  // padding rows: treated as seeing every key
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[j][ks] = bf16x8{};
-    if (act[j] && row < p.rows) {
-      const int node = row / p.group;
-      const int hl = row - node * p.group;
-      node_of[j] = node;
-      const __bf16* qp = q + (((size_t)b * p.n + node) * p.hq + (size_t)g * p.group + hl) * D + 8 * lg;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        u32x4 raw;
-        asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(raw) : "v"(qp + 32 * ks) : "memory");
-        qf[j][ks] = as_bf16x8(raw);
-      }
-    }
-  }
-
-  // Then the first tiles start streaming.
-#pragma unroll
-  for (int t = 0; t < kAhead; ++t)
-    if (t < n_tiles) issue(t);
-
-  f32x4 o[TPW][DT];
-  float m_run[TPW], l_run[TPW];
-#pragma unroll
-  for (int j = 0; j < TPW; ++j) {
-    m_run[j] = kNegInf;
-    l_run[j] = 0.f;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) o[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-  const float c = p.scale_log2;
-
-  // ---- one tile, for each of this wave's 16-row tiles j:
-  //   S^T[key][row] = K[key][:] . Q[row][:]   (A = K from LDS, B = Q^T)
-  //   P = exp2(S c - m_run c)                  (online softmax, lazily rescaled)
-  //   O^T[d][row] += V^T[d][key] . P^T[key][row]
-  // The keys of a tile form two halves kk (keys 32 kk .. 32 kk + 31).  A lane
-  // holds row lr and keys 32 kk + 8 lg + 4 sub + i of S^T (value sc[j][kk][sub][i]).
-  //
-  // The exponentials are computed against the running reference m_run before
-  // the tile's maximum is known, so that they can be interleaved with matrix
-  // work: those of half 0 with the Q.K MFMAs of half 1, those of half 1 with
-  // the P.V MFMAs of half 0.  Lazy rescaling keeps the reference unless a
-  // score exceeds it by more than 2^kSlack (exp2 units); in that rare case
-  // (always on a split's first tile) the reference moves, O and l are
-  // rescaled, and half 0 is scored again and exponentiated anew.
-  //
-  // Operand reads from LDS run kOpAhead operands ahead of their MFMAs, and
-  // scheduling fences keep each step (one operand's MFMAs plus its share of
-  // VALU work) in place, so the compiler neither regroups the reads (which
-  // would expose their latency) nor separates the VALU work from the MFMAs.
-  constexpr int NKO = 4 * KS;        // K operands per tile: (kk, ks, sub)
-  constexpr int NVO = 2 * DT;        // V operands per tile: (kk, dt)
-  constexpr int kOpAhead = 2;
-  constexpr int NVAL = TPW * 8;      // scores per lane in one half
-  static_assert(NKO / 2 == 2 * KS && NVO / 2 == DT, "operand counts");
-
-  auto tile = [&](auto masked_tag, int t) __attribute__((always_inline)) {
-    constexpr bool masked = decltype(masked_tag)::value;
-    const char* Kt = sRing[t % kStages][0];
-    const char* Vt = sRing[t % kStages][1];
-    const bool is_new = (t == n_ctx_tiles);
-    const int nvalid = is_new ? p.n : min(kKeyTile, k_end - (k_begin + t * kKeyTile));
-
-    auto load_k = [&](int idx) __attribute__((always_inline)) {
-      const int kk = idx / (2 * KS), ks = (idx / 2) % KS, sub = idx % 2;
-      const int krow = 32 * kk + 8 * (lr >> 2) + 4 * sub + (lr & 3);
-      return as_bf16x8(*reinterpret_cast<const u32x4*>(Kt + krow * RB + ((4 * ks + lg) ^ swz<D>(krow)) * 16));
-    };
-    // V^T operand of (kk, dt): two transposed 8-byte reads, rows vrow and vrow + 4.
-    // ds_read_b64_tr_b16: in each 16-lane group, lane jl reads row key0 + (jl>>2),
-    // columns d0 + 4*(jl&3) .. +3, and receives V[key0 + i][d0 + jl] for i = 0..3.
-    auto load_v = [&](int idx) __attribute__((always_inline)) {
-      const int kk = idx / DT, dt = idx % DT;
-      const int vrow = 32 * kk + 8 * lg + (lr >> 2);
-      const int chunk = 2 * dt + ((lane & 3) >> 1);
-      const int half = (lane & 1) * 8;
-      const char* va_lo = Vt + vrow * RB + (chunk ^ swz<D>(vrow)) * 16 + half;
-      const char* va_hi = Vt + (vrow + 4) * RB + (chunk ^ swz<D>(vrow + 4)) * 16 + half;
-      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va_lo));
-      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(va_hi));
-      // whole-vector reinterpretation: element-wise bf16 inserts of the 16-bit
-      // lanes were miscompiled (every element became lo[0])
-      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    };
-
-    f32x4 sc[TPW][2][2];
-    bf16x8 kr[kOpAhead + 1];
-    auto qk_step = [&](int idx) __attribute__((always_inline)) {
-      if (idx + kOpAhead < NKO) kr[(idx + kOpAhead) % (kOpAhead + 1)] = load_k(idx + kOpAhead);
-      const int kk = idx / (2 * KS), ks = (idx / 2) % KS, sub = idx % 2;
-#pragma unroll
-      for (int j = 0; j < TPW; ++j)
-        sc[j][kk][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[idx % (kOpAhead + 1)], qf[j][ks],
-                                                                ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sc[j][kk][sub],
-                                                                0, 0, 0);
-    };
-    // Q.K^T of half kk alone (used again by the rescale path)
-    auto qk_half = [&](int kk) __attribute__((always_inline)) {
-#pragma unroll
-      for (int i = 0; i < kOpAhead; ++i) kr[(kk * 2 * KS + i) % (kOpAhead + 1)] = load_k(kk * 2 * KS + i);
-#pragma unroll
-      for (int n = 0; n < 2 * KS; ++n) {
-        const int idx = kk * 2 * KS + n;
-        if (n + kOpAhead < 2 * KS) kr[(idx + kOpAhead) % (kOpAhead + 1)] = load_k(idx + kOpAhead);
-        const int ks = n / 2, sub = n % 2;
-#pragma unroll
-        for (int j = 0; j < TPW; ++j)
-          sc[j][kk][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              kr[idx % (kOpAhead + 1)], qf[j][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sc[j][kk][sub], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    };
-
-    auto mask_half = [&](int kk) __attribute__((always_inline)) {
-      if (!masked) return;
-#pragma unroll
-      for (int j = 0; j < TPW; ++j) {
-        unsigned long long anc = ~0ull;
-        if (TREE && is_new && node_of[j] < p.n) anc = sAnc[node_of[j]];
-#pragma unroll
-        for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int key = 32 * kk + 8 * lg + 4 * sub + i;
-            bool vis = key < nvalid;
-            if (TREE && is_new) vis = vis && ((anc >> key) & 1ull);
-            if (!vis) sc[j][kk][sub][i] = kNegInf;
-          }
-      }
-    };
-
-    float mx[TPW], ls[TPW], neg[TPW];
-#pragma unroll
-    for (int j = 0; j < TPW; ++j) {
-      mx[j] = kNegInf;
-      ls[j] = 0.f;
-      neg[j] = -m_run[j] * c;
-    }
-    // score n of half kk -> probability (argument <= kSlack unless the
-    // reference moves; v_exp_f32 flushes the far tail to 0)
-    auto exp_item = [&](int kk, int n, bool track_max) __attribute__((always_inline)) {
-      const int j = n / 8, sub = (n / 4) % 2, i = n % 4;
-      const float v = sc[j][kk][sub][i];
-      if (track_max) mx[j] = fmaxf(mx[j], v);
-      float e = __builtin_amdgcn_exp2f(fmaf(v, c, neg[j]));
-      // pin the exponential here: the rescale path recomputes half 0, so the
-      // compiler would otherwise sink these below the check, out of the MFMA stream
-      asm volatile("" : "+v"(e));
-      sc[j][kk][sub][i] = e;
-    };
-
-    // Phase 1: Q.K^T of half 0 (matrix work only).
-#pragma unroll
-    for (int i = 0; i < kOpAhead; ++i) kr[i] = load_k(i);
-#pragma unroll
-    for (int idx = 0; idx < NKO / 2; ++idx) {
-      qk_step(idx);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // Phase 2: Q.K^T of half 1, with the exponentials of half 0.
-    mask_half(0);
-#pragma unroll
-    for (int n = 0; n < NKO / 2; ++n) {
-      qk_step(NKO / 2 + n);
-#pragma unroll
-      for (int m = n * NVAL / (NKO / 2); m < (n + 1) * NVAL / (NKO / 2); ++m) exp_item(0, m, true);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // The first V operands stream in while the maximum is checked.
-    bf16x8 vr[kOpAhead + 1];
-#pragma unroll
-    for (int i = 0; i < kOpAhead; ++i) vr[i] = load_v(i);
-    mask_half(1);
-#pragma unroll
-    for (int j = 0; j < TPW; ++j)
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) mx[j] = fmaxf(mx[j], sc[j][1][sub][i]);
-    // Each lane tests its own maximum: no lane above the reference means no row is.
-    bool move = false;
-#pragma unroll
-    for (int j = 0; j < TPW; ++j) move = move | (mx[j] * c > m_run[j] * c + kSlack) | (m_run[j] == kNegInf);
-    if (__builtin_amdgcn_ballot_w64(move)) {
-#pragma unroll
-      for (int j = 0; j < TPW; ++j) {
-        float m = mx[j];
-        m = fmaxf(m, __shfl_xor(m, 16));
-        m = fmaxf(m, __shfl_xor(m, 32));
-        const float m_new = fmaxf(m_run[j], m);
-        const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f((m_run[j] - m_use) * c);
-        m_run[j] = m_use;
-        l_run[j] *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[j][dt] *= alpha;
-        neg[j] = -m_use * c;
-      }
-      // half 0 was exponentiated against the old reference: score it again
-      qk_half(0);
-      mask_half(0);
-#pragma unroll
-      for (int m = 0; m < NVAL; ++m) exp_item(0, m, false);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-
-    // Phase 3: P.V of half 0, with the exponentials of half 1.
-    bf16x8 pb[TPW];
-    // Probabilities of half kk as the bf16 B operand of P.V; the row sum l
-    // is taken from these same bf16 values (two per v_dot2c_f32_bf16), so
-    // numerator and denominator use identical weights.
-    auto to_pb = [&](int kk) __attribute__((always_inline)) {
-      typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
-      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-      for (int j = 0; j < TPW; ++j) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          pb[j][i] = (__bf16)sc[j][kk][0][i];
-          pb[j][4 + i] = (__bf16)sc[j][kk][1][i];
-        }
-        ls[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 0, 1), ones, ls[j], false);
-        ls[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 2, 3), ones, ls[j], false);
-        ls[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 4, 5), ones, ls[j], false);
-        ls[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[j], pb[j], 6, 7), ones, ls[j], false);
-      }
-    };
-    auto pv_step = [&](int idx) __attribute__((always_inline)) {
-      if (idx + kOpAhead < NVO) vr[(idx + kOpAhead) % (kOpAhead + 1)] = load_v(idx + kOpAhead);
-      const int dt = idx % DT;
-#pragma unroll
-      for (int j = 0; j < TPW; ++j)
-        o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vr[idx % (kOpAhead + 1)], pb[j], o[j][dt], 0, 0, 0);
-    };
-    to_pb(0);
-#pragma unroll
-    for (int n = 0; n < DT; ++n) {
-      pv_step(n);
-#pragma unroll
-      for (int m = n * NVAL / DT; m < (n + 1) * NVAL / DT; ++m) exp_item(1, m, false);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // Phase 4: P.V of half 1.
-    to_pb(1);
-#pragma unroll
-    for (int n = 0; n < DT; ++n) {
-      pv_step(DT + n);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int j = 0; j < TPW; ++j) l_run[j] += ls[j];
+  // Ring rule.  Tile t is read by the computing waves' matrix phases: K(t) in
+  // X_t, V(t) in X_{t+1} (see the schedule below); X_{t-1} ends before barrier
+  // t in every wave.  So right after barrier t the stages of K(t - 1) and
+  // V(t - 2) are free, and each wave issues its share of K(t + 3) and V(t + 2)
+  // into them (group t; the prologue issues groups -3, -2, -1: K(0), then
+  // K(1) V(0), then K(2) V(1)).  Barrier t needs K(t) and V(t - 1), both of
+  // group t - 3, so before it each wave waits until at most its groups t - 2
+  // and t - 1 are in flight (vmcnt counts this wave's loads, in issue order).
+  auto ring_issue = [&](int t) __attribute__((always_inline)) {
+    if (t + 3 < n_tiles) issue(t + 3, false);
+    if (t + 2 < n_tiles) issue(t + 2, true);
+  };
+  auto ring_prologue = [&]() __attribute__((always_inline)) {
+    issue(0, false);                    // group -3: K(0)
+    if (n_tiles > 1) issue(1, false);   // group -2: K(1), V(0)
+    issue(0, true);
+    if (n_tiles > 2) issue(2, false);   // group -1: K(2), V(1)
+    if (n_tiles > 1) issue(1, true);
+  };
+  auto ring_wait = [&](int t) __attribute__((always_inline)) {
+    if (t + 2 < n_tiles) wait_vmcnt<4 * SH>();
+    else wait_vmcnt<0>();
   };
 
-  // Queries and parents were issued before the tile loads, so they have
-  // landed once no more than the tile loads are outstanding.  The query
-  // registers pass through the wait so that no use moves above it.
-  if (n_tiles >= kAhead) {
-#pragma unroll
-    for (int j = 0; j < TPW; ++j)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        u32x4 raw = __builtin_bit_cast(u32x4, qf[j][ks]);
-        if (j == 0 && ks == 0)
-          asm volatile("s_waitcnt vmcnt(%1)" : "+v"(raw) : "n"(kAhead * LOADS_PER_TILE) : "memory");
-        else
-          asm volatile("" : "+v"(raw));
-        qf[j][ks] = as_bf16x8(raw);
-      }
-  } else {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
-  if (load_par) {
-    asm volatile("" : "+v"(par_raw));
-    up = (par_raw >= 0 && par_raw < lane) ? par_raw : -1;
-    anc_word = 1ull << lane;
+  if (wave >= p.tiles_rg) {
+    // a wave without rows: streams its share and keeps the barrier count
+    ring_prologue();
+    for (int t = 0; t < n_tiles; ++t) {
+      ring_wait(t);
+      lds_barrier();
+      ring_issue(t);
+    }
+    return;
   }
 
-  if (TREE && has_new && wave == 0) {
+  // =========================== computing waves ===========================
+  const int h = lane >> 5;    // lane half: keys 4h.. of each 8-key group, dims 8h.. of each k-step
+  const int r32 = lane & 31;  // the lane's row within the wave's tile
+  const int row = 32 * (rgi * p.tiles_rg + wave) + r32;  // row of the (b, g) problem
+  const bool row_ok = row < p.rows;
+  const int node = row_ok ? row / p.group : p.n;
+  const int hl = row_ok ? row - node * p.group : 0;
+  const size_t out_row = ((size_t)b * p.n + node) * p.hq + (size_t)g * p.group + hl;
+
+  // Query of the lane's row, dims 16 ks + 8 h .. +7: the B operands of
+  // Q.K^T, and (wave 0, tree) the parents.  Ordinary loads, made to land
+  // before this wave issues its first tile loads: the compiler counts only
+  // the loads it sees, so a wait it placed later would also wait for tile
+  // loads issued in between.
+  bf16x8 qf[KS];
+  {
+    const __bf16* qp = static_cast<const __bf16*>(p.q) + out_row * D + 8 * h;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = row_ok ? *reinterpret_cast<const bf16x8*>(qp + 16 * ks) : bf16x8{};
+  }
+  const bool tree_words = TREE && has_new && wave == 0;
+  int par = -1;
+  if (tree_words && lane < p.n) par = p.parents[(size_t)b * p.n + lane];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) asm volatile("" ::"v"(qf[ks]));  // used here: the loads have landed
+  asm volatile("" ::"v"(par));
+  ring_prologue();
+  ring_wait(0);
+  // ancestor words of the packed tree, anc[i] = {i} u anc[parent(i)], by
+  // pointer doubling in wave 0: after r rounds lane i holds its root path
+  // from i up to (excluding) its 2^r-th ancestor up[i]
+  if (tree_words) {
+    int up = (par >= 0 && par < lane) ? par : -1;
+    unsigned long long anc = 1ull << lane;
 #pragma unroll
     for (int r = 0; r < 6; ++r) {
       const int src = up < 0 ? lane : up;
-      const unsigned lo = __shfl((unsigned)anc_word, src);
-      const unsigned hi = __shfl((unsigned)(anc_word >> 32), src);
+      const unsigned lo = __shfl((unsigned)anc, src);
+      const unsigned hi = __shfl((unsigned)(anc >> 32), src);
       const int up2 = __shfl(up, src);
       if (up >= 0) {
-        anc_word |= ((unsigned long long)hi << 32) | lo;
+        anc |= ((unsigned long long)hi << 32) | lo;
         up = up2;
       }
     }
-    if (lane < p.n) sAnc[lane] = anc_word;  // read after the loop's barriers
+    if (lane < p.n) sAnc[lane] = anc;  // read after the tile barriers
   }
 
-  // Barrier j: every wave's loads of tile j have landed (each wave waits for
-  // its own share first), and the ring stage that tile j + kAhead will use is
-  // free, so the loads of that tile are issued right after it.  (Issuing them
-  // from inside the tile, between the matrix phases, bought no speed and gave
-  // intermittently wrong tree-verify rows, so they stay here.)
-  auto barrier_step = [&](int j) __attribute__((always_inline)) {
-    if (j < n_tiles) {
-      if (j + kAhead - 1 < n_tiles) wait_vmcnt<(kAhead - 1) * LOADS_PER_TILE>();
-      else wait_vmcnt<0>();
-    }
-    lds_barrier();
-    if (j + kAhead < n_tiles) issue(j + kAhead);
+  // LDS read bases.  K operand (kb, ks): row 32 kb + r32, chunk 2 ks + h.
+  // V^T operand (kb, s, db): two transposed reads of rows
+  // 32 kb + 16 s + 4 (gr >> 1) + (jl >> 2) (+ 8), dims 32 db + 16 (gr & 1) +
+  // 4 (jl & 3), gr = lane >> 4, jl = lane & 15: lane l receives
+  // V[key][32 db + l % 32] for the keys 32 kb + 16 s + 4 h + 0..3 (+ 8), the
+  // key order of the score layout.  The swizzle depends on the row modulo 16
+  // only, so all but a per-lane base is an immediate offset (stage, kb, s),
+  // and the tile loop is unrolled over the four stages.
+  const lds_char* kbase[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) kbase[ks] = (const lds_char*)sK + r32 * RB + (((2 * ks + h) ^ swz<D>(r32)) * 16);
+  const lds_char* vbase[DB][2];
+  {
+    const int gr = lane >> 4, jl = lane & 15;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int hi = 0; hi < 2; ++hi) {
+        const int row = 8 * hi + 4 * (gr >> 1) + (jl >> 2);
+        const int chunk = 4 * db + 2 * (gr & 1) + ((jl & 3) >> 1);
+        vbase[db][hi] = (const lds_char*)sV + row * RB + ((chunk ^ swz<D>(row)) * 16) + 8 * (jl & 1);
+      }
+  }
+
+  f32x16 S[2];  // scores of the current tile [key block]
+  f32x16 O[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) O[db] = f32x16{};
+  u32x4 Pw[2][2];  // probabilities as bf16 pairs [key block][16-key k-step]
+  float m_run = kNegInf, l_run = 0.f, nmc = 0.f;
+  const float c = p.scale_log2;
+
+  auto load_k = [&](int ks, int kb, int st) __attribute__((always_inline)) {
+    return __builtin_bit_cast(bf16x8, *(const lds_u32x4*)(kbase[ks] + st * TB + kb * 32 * RB));
+  };
+  auto load_v = [&](int u, int db, int st) __attribute__((always_inline)) {
+    const int off = st * TB + (32 * (u >> 1) + 16 * (u & 1)) * RB;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase[db][0] + off));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase[db][1] + off));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
 
-  // All waves in step: tile t is consumed between barriers t and t + 1 while
-  // kAhead tiles stream behind it.  Full context tiles run first, through a
-  // loop whose body carries no mask; the ragged last context tile and the
-  // new-key tile follow with it.
-  {
-    int t = 0;
-    for (; t < n_full; ++t) {
-      barrier_step(t);
-      if (wave_active) tile(std::false_type{}, t);
+  // scores (kb, j, i = 0..3) -> probabilities into Pw and their sum (from the
+  // same bf16 values that P.V uses, so numerator and denominator match)
+  auto soft_group = [&](int kb, int j, float& lsum) __attribute__((always_inline)) {
+    const float e0 = __builtin_amdgcn_exp2f(fmaf(S[kb][4 * j + 0], c, nmc));
+    const float e1 = __builtin_amdgcn_exp2f(fmaf(S[kb][4 * j + 1], c, nmc));
+    const float e2 = __builtin_amdgcn_exp2f(fmaf(S[kb][4 * j + 2], c, nmc));
+    const float e3 = __builtin_amdgcn_exp2f(fmaf(S[kb][4 * j + 3], c, nmc));
+    const bf16x2 w0 = {(__bf16)e0, (__bf16)e1};
+    const bf16x2 w1 = {(__bf16)e2, (__bf16)e3};
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    lsum = __builtin_amdgcn_fdot2_f32_bf16(w0, ones, lsum, false);
+    lsum = __builtin_amdgcn_fdot2_f32_bf16(w1, ones, lsum, false);
+    Pw[kb][j >> 1][2 * (j & 1)] = __builtin_bit_cast(unsigned, w0);
+    Pw[kb][j >> 1][2 * (j & 1) + 1] = __builtin_bit_cast(unsigned, w1);
+  };
+
+  // Softmax of tile t (phase Y): mask a ragged or new-key tile (key
+  // 32 kb + 8 j + 4 h + i is visible if it is valid and, in the tree, an
+  // ancestor-or-self of the row's node), then the probabilities against the
+  // running reference.  The reference moves to the row maximum when a lane's
+  // probability sum passes kSumLimit (a score more than log2(kSumLimit) / c
+  // above the reference) or there is no reference yet: O and l are rescaled
+  // and the tile's probabilities redone.
+  auto yphase = [&](int t) __attribute__((always_inline)) {
+    const int j = tb + t;
+    const bool is_new = j == ct;
+    const int nvalid = is_new ? p.n : min(64, ctx - 64 * j);
+    if (is_new || nvalid < 64) {
+      unsigned long long anc = ~0ull;
+      if (TREE && is_new && node < p.n) anc = sAnc[node];
+      anc >>= 4 * h;
+      const int lim = nvalid - 4 * h;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int k0 = 32 * kb + 8 * jj + i;  // key - 4 h
+            bool vis = k0 < lim;
+            if (TREE && is_new) vis = vis && ((anc >> k0) & 1ull);
+            if (!vis) S[kb][4 * jj + i] = kNegInf;
+          }
     }
-    for (; t < n_tiles; ++t) {
-      barrier_step(t);
-      if (wave_active) tile(std::true_type{}, t);
+    float lsum = 0.f;
+#pragma unroll
+    for (int g8 = 0; g8 < 8; ++g8) soft_group(g8 >> 2, g8 & 3, lsum);
+    if (__builtin_amdgcn_ballot_w64(lsum > kSumLimit || m_run == kNegInf)) {
+      float mx = kNegInf;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[kb][i]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx);
+      const float m_use = m_new == kNegInf ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_use) * c);
+      m_run = m_use;
+      nmc = -m_use * c;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) O[db] *= alpha;
+      lsum = 0.f;
+#pragma unroll
+      for (int g8 = 0; g8 < 8; ++g8) soft_group(g8 >> 2, g8 & 3, lsum);
     }
+    l_run += lsum;
+  };
+
+  // Matrix phase X: Q.K^T of tile t from stage SK into S (if QK_) and P.V of
+  // tile t - 1 from stage SV (if PV_), one MFMA of each in turn, operands two
+  // ahead.
+  auto xphase = [&](auto SK_, auto QK_, auto PV_) __attribute__((always_inline)) {
+    constexpr int SK = decltype(SK_)::value, SV = (SK + kStages - 1) % kStages;
+    constexpr bool DO_QK = decltype(QK_)::value, DO_PV = decltype(PV_)::value;
+    constexpr int NK = 2 * KS, NV = 4 * DB, NS = NK > NV ? NK : NV;
+    constexpr int AH = kOperandsAhead;
+    bf16x8 kr[NK], vr[NV];
+#pragma unroll
+    for (int i = 0; i < AH; ++i) {
+      if (DO_QK && i < NK) kr[i] = load_k(i >> 1, i & 1, SK);
+      if (DO_PV && i < NV) vr[i] = load_v(i / DB, i % DB, SV);
+    }
+#if GLANCE_XPRIO
+    __builtin_amdgcn_s_setprio(1);
+#endif
+#pragma unroll
+    for (int idx = 0; idx < NS; ++idx) {
+      if (DO_QK && idx < NK) {
+        if (idx + AH < NK) kr[idx + AH] = load_k((idx + AH) >> 1, (idx + AH) & 1, SK);
+        const int ks = idx >> 1, kb = idx & 1;
+        S[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[idx], qf[ks], ks == 0 ? f32x16{} : S[kb], 0, 0, 0);
+      }
+      if (DO_PV && idx < NV) {
+        if (idx + AH < NV) vr[idx + AH] = load_v((idx + AH) / DB, (idx + AH) % DB, SV);
+        const int u = idx / DB, db = idx % DB;
+        O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vr[idx], __builtin_bit_cast(bf16x8, Pw[u >> 1][u & 1]),
+                                                        O[db], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#if GLANCE_XPRIO
+    __builtin_amdgcn_s_setprio(0);
+#endif
+  };
+
+  // Schedule.  X_t = {Q.K^T of tile t, P.V of tile t - 1}, Y_t = softmax of
+  // tile t; every wave runs barrier 0, X_0 Y_0, barrier 1, X_1 Y_1, ...,
+  // X_{n-1} Y_{n-1} and the last P.V.  All waves keep the same order: the two
+  // waves of a SIMD drift apart by themselves and overlap one's matrix phase
+  // with the other's vector phase, which a fixed rotation of half the waves
+  // (lower waves X then Y, upper waves Y then X) did worse, since it put a
+  // barrier between the phases of every other wave.
+  //
+  // Ring invariant: stage s = t % 4 of the ring holds K(t) from its issue
+  // after barrier t - 3 and V(t) from its issue after barrier t - 2.  K(t) is
+  // read in X_t only (between barriers t and t + 1), V(t) in X_{t+1} only
+  // (between barriers t + 1 and t + 2).  The issue after barrier t writes
+  // K(t + 3) and V(t + 2) over K(t - 1) and V(t - 2), whose last reads were
+  // in X_{t-1}, which every wave ended before it arrived at barrier t.
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using YES = std::true_type;
+  using NO = std::false_type;
+  lds_barrier();  // barrier 0 (its wait came with the query's): K(0) has landed, the ancestor words are written
+  ring_issue(0);
+  xphase(I0{}, YES{}, NO{});
+  auto step = [&](int t, auto SK_) __attribute__((always_inline)) {
+    yphase(t - 1);
+    ring_wait(t);   // this wave's own DMA of K(t) and V(t - 1) is complete
+    lds_barrier();  // barrier t: every wave's is, and X_{t-1} has ended everywhere
+    ring_issue(t);
+    xphase(SK_, YES{}, YES{});
+  };
+  int t = 1;
+  while (t < n_tiles) {
+    step(t, I1{});
+    if (++t >= n_tiles) break;
+    step(t, I2{});
+    if (++t >= n_tiles) break;
+    step(t, I3{});
+    if (++t >= n_tiles) break;
+    step(t, I0{});
+    ++t;
+  }
+  yphase(n_tiles - 1);
+  switch (n_tiles & 3) {  // P.V of the last tile, stage (n_tiles - 1) % 4
+    case 1: xphase(I1{}, NO{}, YES{}); break;
+    case 2: xphase(I2{}, NO{}, YES{}); break;
+    case 3: xphase(I3{}, NO{}, YES{}); break;
+    default: xphase(I0{}, NO{}, YES{}); break;
   }
 
-  // ---- partial results of this split: O unnormalised, (max * c, sum).
+  l_run += __shfl_xor(l_run, 32);  // lanes l and l + 32 hold the same row
+  float M = m_run * c;             // reference in log2 units
+  float lsum = l_run;
+
+  if (split) {
+    // partial of this piece: O in the MFMA layout (one float4 per lane per
+    // store, 1 KB per wave-wide store), then (max * c, sum) per row
+    const size_t ws = ((size_t)g * p.slots_per_g + pc.first + pc.index) * p.row_groups + rgi;
+    float4* po = reinterpret_cast<float4*>(p.part_o) + (ws * p.tiles_rg + wave) * (OV / 4) * 64 + lane;
 #pragma unroll
-  for (int j = 0; j < TPW; ++j) {
-    if (!act[j]) continue;
-    float l = l_run[j];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    const int row = (tile0 + j) * 16 + lr;
-    const size_t pr = (((size_t)b * p.hkv + g) * p.nsplit + s) * p.rows_pad + row;
-    if (lg == 0) p.part_ml[pr] = make_float2(m_run[j] * c, l);
-    float* po = p.part_o + pr * D + 4 * lg;
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4*>(po + 16 * dt) = o[j][dt];
+      for (int j = 0; j < 4; ++j)
+        po[(db * 4 + j) * 64] = make_float4(O[db][4 * j], O[db][4 * j + 1], O[db][4 * j + 2], O[db][4 * j + 3]);
+    if (h == 0) p.part_ml[ws * p.rows_rg + 32 * wave + r32] = make_float2(M, lsum);
+    return;
   }
+
+  // output: lane l holds O^T[32 db + 8 j + 4 h + i][row], i = 0..3 consecutive dims
+  if (!row_ok) return;
+  const float inv = 1.f / lsum;
+  __bf16* op = static_cast<__bf16*>(p.out) + out_row * D + 4 * h;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bf16x4 o = {(__bf16)(O[db][4 * j] * inv), (__bf16)(O[db][4 * j + 1] * inv),
+                        (__bf16)(O[db][4 * j + 2] * inv), (__bf16)(O[db][4 * j + 3] * inv)};
+      *reinterpret_cast<bf16x4*>(op + 32 * db + 8 * j) = o;
+    }
+  if (p.lse && h == 0) p.lse[out_row] = (M + __builtin_amdgcn_logf(lsum)) * kLn2;
 }
 
 int grid_blocks(const AttnParams& p) {
-  const int groups = p.nsplit * p.batch * p.hkv;
-  return ((groups + 7) / 8) * 8 * p.row_groups;
-}
-
-template <int D, bool TREE>
-void launch_d(const AttnParams& p, hipStream_t s) {
-  const dim3 grid(grid_blocks(p)), block(kBf16Waves * 64);
-  if (p.tiles_per_wave == 2) hipLaunchKernelGGL((attn_bf16_partial<D, TREE, 2>), grid, block, 0, s, p);
-  else hipLaunchKernelGGL((attn_bf16_partial<D, TREE, 1>), grid, block, 0, s, p);
+  const int slots = p.slots_per_g * p.hkv;
+  return ((slots + 7) / 8) * 8 * p.row_groups;
 }
 
 }  // namespace
 
 hipError_t launch_attn_bf16(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const dim3 grid(grid_blocks(p)), block(512);
   if (ev0) (void)hipEventRecord(ev0, s);
   if (p.d == 128) {
-    if (tree) launch_d<128, true>(p, s);
-    else launch_d<128, false>(p, s);
+    if (tree) hipLaunchKernelGGL((attn_bf16<128, true>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((attn_bf16<128, false>), grid, block, 0, s, p);
   } else {
-    if (tree) launch_d<64, true>(p, s);
-    else launch_d<64, false>(p, s);
+    if (tree) hipLaunchKernelGGL((attn_bf16<64, true>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((attn_bf16<64, false>), grid, block, 0, s, p);
   }
   hipError_t e = hipGetLastError();
   if (ev1) (void)hipEventRecord(ev1, s);

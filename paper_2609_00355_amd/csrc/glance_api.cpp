@@ -37,26 +37,23 @@ bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Default split size: aim at about one workgroup per compute unit over the
-// whole grid, with at least 256 and at most 8192 context keys per split.
-int auto_split_keys(const glance_attn_shape& s, int row_groups) {
-  long long target_wgs = 256;
-  if (const char* e = getenv("GLANCE_TARGET_WGS")) {  // tuning override
-    const long long v = atoll(e);
-    if (v >= 8 && v <= (1 << 20)) target_wgs = v;
-  }
+// fp32 kernel: context keys per split, about one workgroup per compute unit
+// over the whole grid, at least 256 and at most 8192 keys per split.
+int f32_split_keys(const glance_attn_shape& s, int row_groups) {
   const long long cap = s.ctx_capacity > 0 ? s.ctx_capacity : 1;
-  long long per = cap * s.batch * s.n_kv_heads * row_groups / target_wgs;
+  long long per = cap * s.batch * s.n_kv_heads * row_groups / 256;
   per = (per + glance::kKeyTile - 1) / glance::kKeyTile * glance::kKeyTile;
   if (per < 256) per = 256;
   if (per > 8192) per = 8192;
   return (int)per;
 }
 
+// Attention workspace: [piece table][(max, sum) partials][O partials].
 struct Plan {
   glance::AttnParams p;
-  size_t part_o_bytes;
+  size_t counter_bytes;  // the bf16 path's per-sequence piece table
   size_t part_ml_bytes;
+  size_t part_o_bytes;
   size_t total;
 };
 
@@ -77,9 +74,6 @@ glance_status check_shape(const glance_attn_shape* s) {
   if (s->ctx_capacity < 0) return fail(GLANCE_ERR_INVALID_ARG, "ctx_capacity must be >= 0");
   if (s->dtype != GLANCE_F32 && s->dtype != GLANCE_BF16)
     return fail(GLANCE_ERR_UNSUPPORTED, "dtype must be GLANCE_F32 or GLANCE_BF16");
-  if (s->split_keys < 0 || s->split_keys % glance::kKeyTile != 0)
-    return fail(GLANCE_ERR_INVALID_ARG, "split_keys must be 0 or a positive multiple of %d (got %d)",
-                glance::kKeyTile, s->split_keys);
   if (!(s->sm_scale == s->sm_scale) || isinf(s->sm_scale))
     return fail(GLANCE_ERR_INVALID_ARG, "sm_scale must be finite");
   // index arithmetic in the kernels: element offsets fit in 64 bits, per-tensor
@@ -101,35 +95,35 @@ glance_status make_plan(const glance_attn_shape* s, Plan* out) {
   p.cap = s->ctx_capacity;
   p.d = s->head_dim;
   p.rows = p.n * p.group;
-  if (s->dtype == GLANCE_BF16) {
-    // 16-row tiles: one per wave when they all fit in one workgroup, else two
-    // per wave (each K/V operand read from LDS then feeds two MFMAs), spread
-    // evenly over the fewest row groups.
-    const int tiles = (p.rows + 15) / 16;
-    p.tiles_per_wave = tiles <= glance::kBf16Waves ? 1 : glance::kBf16MaxTilesPerWave;
-    if (const char* e = getenv("GLANCE_TILES_PER_WAVE")) {  // tuning override
-      const int v = atoi(e);
-      if (v == 1 || v == 2) p.tiles_per_wave = v;
-    }
-    const int per_group_max = glance::kBf16Waves * p.tiles_per_wave;
-    p.row_groups = (tiles + per_group_max - 1) / per_group_max;
-    p.tiles_per_group = (tiles + p.row_groups - 1) / p.row_groups;
-    p.rows_pad = tiles * 16;
-  } else {
-    p.row_groups = (p.rows + glance::kF32RowBlock - 1) / glance::kF32RowBlock;
-    p.tiles_per_group = 0;
-    p.tiles_per_wave = 0;
-    p.rows_pad = p.row_groups * glance::kF32RowBlock;
-  }
-  p.split_keys = s->split_keys > 0 ? s->split_keys : auto_split_keys(*s, p.row_groups);
-  p.nsplit = p.cap > 0 ? (p.cap + p.split_keys - 1) / p.split_keys : 1;
   const float scale = s->sm_scale > 0.f ? s->sm_scale : 1.0f / sqrtf((float)s->head_dim);
   p.scale_log2 = scale * 1.4426950408889634f;
-  const size_t slots = (size_t)p.batch * p.hkv * p.nsplit * p.rows_pad;
   Plan pl;
-  pl.part_o_bytes = round_up(slots * p.d * sizeof(float), 256);
-  pl.part_ml_bytes = round_up(slots * sizeof(float2), 256);
-  pl.total = pl.part_o_bytes + pl.part_ml_bytes;
+  if (s->dtype == GLANCE_BF16) {
+    // Row groups of at most seven 32-row tiles (seven computing waves and
+    // the streaming wave), spread evenly; about one workgroup per compute
+    // unit (256) over all piece slots, at least one slot per sequence.
+    const int tiles = (p.rows + 31) / 32;
+    p.row_groups = (tiles + 6) / 7;
+    p.tiles_rg = (tiles + p.row_groups - 1) / p.row_groups;
+    p.rows_rg = 32 * p.tiles_rg;
+    const int per_g = 256 / (p.hkv * p.row_groups);
+    p.slots_per_g = per_g > p.batch ? per_g : p.batch;
+    p.min_tiles = 4;
+    const size_t wslots = (size_t)p.slots_per_g * p.hkv * p.row_groups;
+    pl.counter_bytes = round_up((size_t)p.batch * sizeof(int2), 256);
+    pl.part_ml_bytes = round_up(wslots * p.rows_rg * sizeof(float2), 256);
+    pl.part_o_bytes = round_up(wslots * p.rows_rg * p.d * sizeof(float), 256);
+  } else {
+    p.row_groups = (p.rows + glance::kF32RowBlock - 1) / glance::kF32RowBlock;
+    p.rows_pad = p.row_groups * glance::kF32RowBlock;
+    p.split_keys = f32_split_keys(*s, p.row_groups);
+    p.nsplit = p.cap > 0 ? (p.cap + p.split_keys - 1) / p.split_keys : 1;
+    const size_t slots = (size_t)p.batch * p.hkv * p.nsplit * p.rows_pad;
+    pl.counter_bytes = 0;
+    pl.part_ml_bytes = round_up(slots * sizeof(float2), 256);
+    pl.part_o_bytes = round_up(slots * p.d * sizeof(float), 256);
+  }
+  pl.total = pl.counter_bytes + pl.part_ml_bytes + pl.part_o_bytes;
   pl.p = p;
   *out = pl;
   return ok();
@@ -185,17 +179,22 @@ glance_status attn_common(bool tree, const glance_attn_shape* s, const void* q, 
   p.v_new = v_new;
   p.ctx_lens = ctx_lens;
   p.parents = tree ? parents : nullptr;
-  p.part_o = static_cast<float*>(workspace);
-  p.part_ml = reinterpret_cast<float2*>(static_cast<char*>(workspace) + pl.part_o_bytes);
+  char* ws = static_cast<char*>(workspace);
+  p.plan = pl.counter_bytes ? reinterpret_cast<int2*>(ws) : nullptr;
+  p.part_ml = reinterpret_cast<float2*>(ws + pl.counter_bytes);
+  p.part_o = reinterpret_cast<float*>(ws + pl.counter_bytes + pl.part_ml_bytes);
   p.out = out;
   p.lse = lse;
   hipEvent_t e0, e1;
   take_events(&e0, &e1);
-  const bool bf16 = s->dtype == GLANCE_BF16;
-  hipError_t e = bf16 ? glance::launch_attn_bf16(p, tree, stream, e0, e1)
-                      : glance::launch_attn_f32(p, tree, stream, e0, e1);
+  // the profiling events bracket the whole call: attention pass and merge pass
+  if (e0) (void)hipEventRecord(e0, stream);
+  hipError_t e = s->dtype == GLANCE_BF16 ? glance::launch_attn_bf16(p, tree, stream, nullptr, nullptr)
+                                         : glance::launch_attn_f32(p, tree, stream, nullptr, nullptr);
   if ((st = check_hip(e, "attention kernel launch")) != GLANCE_OK) return st;
-  e = glance::launch_attn_merge(p, bf16, stream);
+  e = s->dtype == GLANCE_BF16 ? glance::launch_attn_merge_pieces(p, stream)
+                              : glance::launch_attn_merge(p, false, stream);
+  if (e1) (void)hipEventRecord(e1, stream);
   return check_hip(e, "merge kernel launch");
 }
 
@@ -213,11 +212,7 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
   const long long rows = (long long)batch * n_nodes;
   if (rows * (long long)vocab > (1LL << 40)) return fail(GLANCE_ERR_UNSUPPORTED, "logits too large");
   // about 512 workgroups over the grid (two per CU), chunks of at least 8192 values
-  long long target = 512;
-  if (const char* e = getenv("GLANCE_ACCEPT_WGS")) {  // tuning override
-    const long long v = atoll(e);
-    if (v >= 1 && v <= (1 << 20)) target = v;
-  }
+  const long long target = 512;
   long long chunks = (target + rows - 1) / rows;
   long long max_chunks = ((long long)vocab + 8191) / 8192;
   if (chunks > max_chunks) chunks = max_chunks;
@@ -230,11 +225,7 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
   // sampling: about 2048 workgroups (eight waves a SIMD; measured best of
   // 512..4096 at 256 x 152064 bf16), chunks a multiple of 1024 tokens so that
   // only a row's last chunk has a ragged tail
-  long long s_target = 2048;
-  if (const char* e = getenv("GLANCE_SAMPLE_WGS")) {  // tuning override
-    const long long v = atoll(e);
-    if (v >= 1 && v <= (1 << 20)) s_target = v;
-  }
+  const long long s_target = 2048;
   long long s_chunks = (s_target + rows - 1) / rows;
   const long long s_max = ((long long)vocab + 4095) / 4096;
   if (s_chunks > s_max) s_chunks = s_max;
@@ -553,7 +544,8 @@ glance_status glance_commit_path(int32_t batch, int32_t n_nodes, int32_t n_kv_he
   return check_hip(glance::launch_commit(p, stream, e0, e1), "commit kernel launch");
 }
 
-size_t glance_attn_workspace_size(const glance_attn_shape* s) {
+size_t glance_attn_workspace_size(const glance_attn_shape* s, int32_t is_verify) {
+  (void)is_verify;  // the draft and the verify of one shape share a plan
   Plan pl;
   if (make_plan(s, &pl) != GLANCE_OK) return 0;
   return pl.total;

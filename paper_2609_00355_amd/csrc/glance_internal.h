@@ -13,16 +13,14 @@ constexpr int kWaves = 4;
 // Rows per workgroup of the fp32 attention kernel (kWaves waves x 8 rows).
 constexpr int kF32RowsPerWave = 8;
 constexpr int kF32RowBlock = kWaves * kF32RowsPerWave;
-// Waves per workgroup of the bf16 matrix-core kernel (two per SIMD) and the
-// most 16-row tiles one of its waves holds.
-constexpr int kBf16Waves = 8;
-constexpr int kBf16MaxTilesPerWave = 2;
 
 // Everything a split-KV attention launch needs.  Layouts:
 //   q      [batch][n][hq][d]         k_ctx/v_ctx [batch][hkv][cap][d]
 //   k_new  [batch][n][hkv][d]        parents [batch][n]
-//   part_o [batch][hkv][nsplit][rows_pad][d] f32 (unnormalised partial output)
-//   part_ml[batch][hkv][nsplit][rows_pad]    f32x2 (running max * scale*log2e, sum)
+//   part_o  fp32 kernel: [batch][hkv][nsplit][rows_pad][d] f32 (unnormalised partial output)
+//           bf16 kernel: [slot * row_groups + rg][tiles_rg][d / 8][64 lanes] f32x4 (MFMA layout)
+//   part_ml fp32 kernel: [batch][hkv][nsplit][rows_pad] f32x2 (running max * scale*log2e, sum)
+//           bf16 kernel: [slot * row_groups + rg][rows_rg] f32x2
 //   out    [batch][n][hq][d]         lse [batch][n][hq]
 // Row r of a (sequence, KV head) problem is new row r / group of query head
 // g * group + r % group.
@@ -40,13 +38,17 @@ struct AttnParams {
   float* lse;
   int batch, n, hq, hkv, group, cap, d;
   int rows;       // n * group
-  int rows_pad;   // rows rounded up to the kernel's row block
-  int row_groups; // workgroups sharing one KV split
-  int tiles_per_group;  // 16-row tiles per row group (bf16 kernel)
-  int tiles_per_wave;   // 16-row tiles per wave, 1 or 2 (bf16 kernel)
-  int nsplit;     // split slots per (sequence, KV head) = ceil(cap / split_keys), >= 1
-  int split_keys; // context keys per split, multiple of kKeyTile
+  int rows_pad;   // rows rounded up to the kernel's row block (fp32 kernel)
+  int row_groups; // workgroups sharing one run of key tiles
+  int nsplit;     // split slots per (sequence, KV head) = ceil(cap / split_keys), >= 1 (fp32 kernel)
+  int split_keys; // context keys per split, multiple of kKeyTile (fp32 kernel)
   float scale_log2;  // sm_scale * log2(e)
+  // bf16 kernel: pieces planned on the device from ctx_lens (see attn_bf16.hip)
+  int slots_per_g;  // piece slots per KV head (>= batch)
+  int min_tiles;    // smallest piece, in 64-key tiles
+  int tiles_rg;     // 32-row tiles per row group (= computing waves, 1..7)
+  int rows_rg;      // 32 * tiles_rg
+  int2* plan;       // [batch] (pieces, first piece slot) of each sequence, for the merge pass
 };
 
 struct AcceptParams {
@@ -126,6 +128,7 @@ struct CommitParams {
 hipError_t launch_attn_bf16(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_attn_f32(const AttnParams& p, bool tree, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_attn_merge(const AttnParams& p, bool out_bf16, hipStream_t s);
+hipError_t launch_attn_merge_pieces(const AttnParams& p, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_sample(const AcceptParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_tree(const TreeParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);

@@ -35,16 +35,16 @@ def to_dev(d):
     return {k: (v.cuda() if torch.is_tensor(v) else v) for k, v in d.items()}
 
 
-def run_attention(kind, inp, parents=None, split_keys=0, sm_scale=0.0):
+def run_attention(kind, inp, parents=None, sm_scale=0.0, workspace=None):
     dev = to_dev(inp)
     if kind == "draft":
         out, lse = G.glance_block_draft_attn(dev["q"], dev["k_ctx"], dev["v_ctx"], dev["k_new"],
-                                             dev["v_new"], dev["ctx_lens"], split_keys=split_keys,
-                                             sm_scale=sm_scale)
+                                             dev["v_new"], dev["ctx_lens"], sm_scale=sm_scale,
+                                             workspace=workspace)
     else:
         out, lse = G.glance_tree_verify_attn(dev["q"], dev["k_ctx"], dev["v_ctx"], dev["k_new"],
                                              dev["v_new"], dev["ctx_lens"], parents.cuda(),
-                                             split_keys=split_keys, sm_scale=sm_scale)
+                                             sm_scale=sm_scale, workspace=workspace)
     torch.cuda.synchronize()
     return out.float().cpu().numpy(), lse.cpu().numpy()
 

@@ -62,7 +62,6 @@ def _shape(**kw):
     (dict(head_dim=96), G.GLANCE_ERR_UNSUPPORTED),
     (dict(ctx_capacity=-1), G.GLANCE_ERR_INVALID_ARG),
     (dict(dtype=5), G.GLANCE_ERR_UNSUPPORTED),
-    (dict(split_keys=100), G.GLANCE_ERR_INVALID_ARG),
 ])
 def test_bad_shapes_are_rejected(lib, kw, code):
     s = _shape(**kw)
@@ -102,12 +101,24 @@ def test_workspace_checks(lib):
     assert st == G.GLANCE_ERR_WORKSPACE and "256" in G.glance_last_error()
 
 
-def test_workspace_size_scales_with_splits(lib):
-    a = G.glance_attn_workspace_size(_shape(split_keys=1024))
-    b = G.glance_attn_workspace_size(_shape(split_keys=512))
-    assert b > a > 0
-    # partial outputs dominate: splits x rows x head_dim x 4 bytes
-    assert a >= 2 * 112 * 128 * 4
+def test_workspace_size_depends_on_the_shape_only(lib):
+    s = _shape(batch=4, n_new=64, ctx_capacity=16384)
+    a = G.glance_attn_workspace_size(s, 1)
+    assert a == G.glance_attn_workspace_size(s, 0) > 0
+    # 256 workgroups' partials: 32 piece slots x 4 KV heads x 2 row groups,
+    # each 224 rows x head_dim x 4 bytes
+    assert a >= 256 * 224 * 128 * 4
+    # no hidden inputs: the same size in a child process with a changed environment
+    import subprocess
+    import sys
+    env = dict(os.environ, GLANCE_TARGET_WGS="64", GLANCE_TILES_PER_WAVE="1", GLANCE_ACCEPT_WGS="7")
+    code = ("import paper_2609_00355_amd as G; s = G.attn_shape(4, 64, 28, 4, 128, 16384, G.GLANCE_BF16); "
+            "print(G.glance_attn_workspace_size(s, 1), G.glance_accept_workspace_size(4, 64, 152064))")
+    out = subprocess.run([sys.executable, "-c", code], env=env, cwd=ROOT, capture_output=True, text=True, check=True)
+    assert out.stdout.split() == [str(a), str(G.glance_accept_workspace_size(4, 64, 152064))]
+    # more sequences than piece slots: one slot per sequence
+    big = G.glance_attn_workspace_size(_shape(batch=100, n_new=64, ctx_capacity=128), 1)
+    assert big >= 100 * 4 * 2 * 224 * 128 * 4
 
 
 def test_accept_argument_checks(lib):

@@ -27,12 +27,12 @@ def _w(name, **kw):
 
 
 def _check(kind, w, ctx_lens, n, seed=0, variant=None, poison=False, tree_shape="best_first",
-           split_keys=0, cap=None, what=""):
+           cap=None, what="", workspace=None):
     inp = C.attention_inputs(w, kind, n, ctx_lens, seed, variant, poison, cap=cap)
     par = None
     if kind == "verify":
         par, _ = C.tree_inputs(w, seed, tree_shape, n=n, batch=len(ctx_lens))
-    out, lse = run_attention(kind, inp, par, split_keys=split_keys)
+    out, lse = run_attention(kind, inp, par, workspace=workspace)
     ref_out, ref_lse = oracle_attention(kind, inp, par)
     print(f"[{what}] {kind} n={n} ctx={list(ctx_lens)[:4]} variant={variant}", flush=True)
     return assert_close(out, lse, ref_out, ref_lse, w.dtype, what)
@@ -126,7 +126,7 @@ def test_bf16_value_range(kind):
     par = None
     if kind == "verify":
         par, _ = C.tree_inputs(w, 8, "best_first", n=n, batch=2)
-    out, lse = run_attention(kind, inp, par, split_keys=128)
+    out, lse = run_attention(kind, inp, par)
     ref_out, ref_lse = oracle_attention(kind, inp, par)
     assert np.all(np.isfinite(out))
     scale = np.abs(ref_out).max()
@@ -137,12 +137,35 @@ def test_bf16_value_range(kind):
     assert np.abs(lse - ref_lse).max() <= TOL["bf16"]["lse"] * max(1.0, np.abs(ref_lse).max())
 
 
-@pytest.mark.parametrize("split_keys", [64, 256, 1024, 0])
-def test_split_count_invariance(split_keys):
-    w = _w("verify_4k", batch=2)
+# The key pieces are planned on the device from ctx_lens: at 28/4 heads a
+# sequence of ctx keys is cut into about ceil((ctx / 64 + 1) / T) pieces with
+# T >= 4 tiles, so these contexts give one piece (no merge), two, a dozen and
+# several dozen (draft: 64 slots per KV head, verify: 32 per row group).
+@pytest.mark.parametrize("ctx", [100, 300, 3000, 20000])
+def test_piece_count_invariance(ctx):
+    w = _w("verify_4k", batch=1)
     for kind, n in (("draft", 16), ("verify", 64)):
-        _check(kind, w, [3000, 1234], n, seed=8, variant="sharp1", split_keys=split_keys, cap=3100,
-               what=f"split {split_keys}")
+        _check(kind, w, [ctx], n, seed=8, variant="sharp1", cap=ctx + 7, what=f"ctx {ctx}")
+
+
+def test_many_sequences_more_than_slots():
+    """40 sequences > the 32 verify slots per KV head that 256 workgroups
+    would give: the plan takes one slot per sequence at least."""
+    w = _w("verify_4k", batch=40)
+    rng = np.random.default_rng(12)
+    ctx = [int(x) for x in rng.integers(0, 700, size=40)]
+    for kind, n in (("draft", 16), ("verify", 64)):
+        _check(kind, w, ctx, n, seed=12, variant="sharp1", poison=True, cap=720, what="40 sequences")
+
+
+def test_workspace_reuse_across_shapes():
+    """One workspace serves calls of different shapes in turn: every call
+    leaves its arrival counters at zero for the next."""
+    w = _w("verify_4k", batch=2)
+    ws = torch.zeros(64 << 20, dtype=torch.uint8, device="cuda")
+    for ctx, n, kind in (([3000, 1234], 64, "verify"), ([900, 20], 16, "draft"), ([5000, 4000], 64, "verify"),
+                         ([3000, 1234], 16, "draft")):
+        _check(kind, w, ctx, n, seed=13, variant="sharp1", cap=5100, what=f"reuse {kind} {ctx}", workspace=ws)
 
 
 def test_ragged_batch_small():
