@@ -17,6 +17,8 @@
  *                            walk of Algorithm 1: the longest root-to-node path
  *                            whose every edge carries the parent row's argmax,
  *                            plus the bonus token that becomes the next root;
+ *   glance_greedy_accept_entropy  the same, plus the entropy of each root row
+ *                            (the predictor of Sec. 4's entropy law);
  *   glance_sample_accept     the same walk under sampling at temperature T:
  *                            each row's token is a Gumbel-max draw from
  *                            softmax(z / T) with counter-based noise;
@@ -157,12 +159,8 @@ glance_status glance_tree_verify_attn(const glance_attn_shape* s, const void* q,
  *   next_root   device [batch] int32: the bonus token argmax_out[b][last node],
  *               which the round commits after the a accepted tokens and which
  *               becomes the next round's root.
- *   root_entropy device [batch] float32, or NULL: the entropy (nats) of the
- *               softmax of row 0, the target's next-token distribution at the
- *               round root -- the scalar the paper's entropy law (Sec. 4)
- *               predicts acceptance from.  Computed in the argmax pass (fp32
- *               sums relative to each chunk's maximum); -inf logits carry
- *               probability 0; undefined if row 0 holds a NaN or +inf.
+ *   workspace   device, >= glance_accept_workspace_size(batch, n_nodes, vocab)
+ *               bytes, 256-byte aligned
  * Walk: v = 0; t = argmax(row v); if some child c of v has tokens[c] == t
  * (lowest such c if siblings repeat a token), append c and continue from c,
  * else stop.  Each step moves to a larger node index, so the walk ends within
@@ -173,8 +171,26 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    glance_dtype logits_dtype, const void* logits,
                                    const int32_t* parents, const int32_t* tokens,
                                    int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
-                                   int32_t path_stride, int32_t* next_root, float* root_entropy,
+                                   int32_t path_stride, int32_t* next_root,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * glance_greedy_accept plus the root entropy (Sec. 4's entropy law predicts
+ * the accepted length from the target's next-token entropy at the round
+ * root):
+ *   root_entropy device [batch] float32, not NULL: the entropy (nats) of the
+ *               softmax of row 0 of each sequence.  Computed in the same
+ *               launch (fp32 sums relative to each chunk's maximum; the root
+ *               row's workgroups read their chunk a second time); -inf logits
+ *               carry probability 0; undefined if row 0 holds a NaN or +inf.
+ * All other arguments, outputs and the workspace as for glance_greedy_accept.
+ */
+glance_status glance_greedy_accept_entropy(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                           glance_dtype logits_dtype, const void* logits,
+                                           const int32_t* parents, const int32_t* tokens,
+                                           int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
+                                           int32_t path_stride, int32_t* next_root, float* root_entropy,
+                                           void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Sampling acceptance at temperature T > 0 (the Limitations section: under
@@ -305,9 +321,10 @@ size_t glance_tree_workspace_size(int32_t batch, int32_t horizon, int32_t vocab,
  * is_verify = 0 for glance_block_draft_attn, 1 for glance_tree_verify_attn.
  * The two sizes are equal in this build, so one workspace serves both calls
  * of a shape.  The size depends on the shape only. Host only. */
-size_t glance_attn_workspace_size(const glance_attn_shape* s, int32_t is_verify);
+size_t glance_attn_workspace_size(const glance_attn_shape* s, int is_verify);
 
-/* Workspace bytes glance_greedy_accept needs (0 if the sizes are invalid). Host only. */
+/* Workspace bytes glance_greedy_accept, glance_greedy_accept_entropy and
+ * glance_sample_accept need (0 if the sizes are invalid).  Host only. */
 size_t glance_accept_workspace_size(int32_t batch, int32_t n_nodes, int32_t vocab);
 
 /*

@@ -57,7 +57,9 @@ _SIGS = {
     "glance_tree_verify_attn": (ctypes.c_int, [ctypes.POINTER(AttnShape), _P, _P, _P, _P, _P, _P, _P, _P,
                                                _P, _P, _SZ, _P]),
     "glance_greedy_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P, _P, _I32,
-                                            _P, _P, _P, _SZ, _P]),
+                                            _P, _P, _SZ, _P]),
+    "glance_greedy_accept_entropy": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P, _P,
+                                                    _I32, _P, _P, _P, _SZ, _P]),
     "glance_sample_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, ctypes.c_float,
                                             ctypes.c_uint64, ctypes.c_uint32, _P, _P, _P, _P, _I32, _P, _P,
                                             _SZ, _P]),
@@ -66,7 +68,7 @@ _SIGS = {
     "glance_tree_workspace_size": (_SZ, [_I32, _I32, _I32, _I32]),
     "glance_commit_path": (ctypes.c_int, [_I32, _I32, _I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _I32, _P,
                                           _P, _P, _P]),
-    "glance_attn_workspace_size": (_SZ, [ctypes.POINTER(AttnShape), _I32]),
+    "glance_attn_workspace_size": (_SZ, [ctypes.POINTER(AttnShape), ctypes.c_int]),
     "glance_accept_workspace_size": (_SZ, [_I32, _I32, _I32]),
     "glance_validate_tree": (ctypes.c_int, [_I32, _P, _P, _I32]),
     "glance_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -273,14 +275,19 @@ def glance_tree_verify_attn(q, k_ctx, v_ctx, k_new, v_new, ctx_lens, parents, ou
 def glance_greedy_accept(logits, parents, tokens, path_stride=None, outputs=None, workspace=None,
                          stream=None, want_entropy=False):
     """Row argmax + the walk of Algorithm 1.  Returns a dict of GPU tensors (int32, and
-    float32 root_entropy [batch] when want_entropy)."""
+    float32 root_entropy [batch] when want_entropy, which calls
+    glance_greedy_accept_entropy)."""
     args, outputs, _ = _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream,
                                     want_entropy)
-    _check(lib().glance_greedy_accept(*args))
+    _check(_accept_fn(want_entropy)(*args))
     return outputs
 
 
-def _accept_common(logits, parents, tokens, path_stride, outputs, workspace, rows_key):
+def _accept_fn(want_entropy):
+    return lib().glance_greedy_accept_entropy if want_entropy else lib().glance_greedy_accept
+
+
+def _accept_common(logits, parents, tokens, path_stride, outputs, workspace, rows_key, stream):
     """Checks and outputs shared by both acceptances; `rows_key` names the per-row output."""
     torch = _torch()
     _dev(logits, "logits", ndim=3)
@@ -293,16 +300,14 @@ def _accept_common(logits, parents, tokens, path_stride, outputs, workspace, row
     path_stride = int(path_stride or n)
     dev = logits.device
     if outputs is None:
-        outputs = {
-            rows_key: torch.empty((batch, n), dtype=torch.int32, device=dev),
-            "accept_len": torch.empty((batch,), dtype=torch.int32, device=dev),
-            "accept_path": torch.empty((batch, path_stride), dtype=torch.int32, device=dev),
-            "next_root": torch.empty((batch,), dtype=torch.int32, device=dev),
-        }
+        def new(shape):
+            return _new_output(torch.empty, shape, stream, dtype=torch.int32, device=dev)
+        outputs = {rows_key: new((batch, n)), "accept_len": new((batch,)), "accept_path": new((batch, path_stride)),
+                   "next_root": new((batch,))}
     need = glance_accept_workspace_size(batch, n, vocab)
     if need == 0:
         raise GlanceError(GLANCE_ERR_INVALID_ARG, glance_last_error())
-    ws = _workspace(need, dev, workspace)
+    ws = _workspace(need, dev, workspace, stream)
     head = [ctypes.c_int32(batch), ctypes.c_int32(n), ctypes.c_int32(vocab), ctypes.c_int(code), _ptr(logits),
             _ptr(parents), _ptr(tokens)]
     walk = [_ptr(outputs["accept_len"]), _ptr(outputs["accept_path"]), ctypes.c_int32(path_stride),
@@ -314,11 +319,12 @@ def _accept_common(logits, parents, tokens, path_stride, outputs, workspace, row
 def _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream, want_entropy):
     torch = _torch()
     head, walk, tail, outputs, ws = _accept_common(logits, parents, tokens, path_stride, outputs, workspace,
-                                                   "argmax")
+                                                   "argmax", stream)
     if want_entropy and outputs.get("root_entropy") is None:
-        outputs["root_entropy"] = torch.empty((logits.shape[0],), dtype=torch.float32, device=logits.device)
-    args = head + [_ptr(outputs["argmax"])] + walk + [_ptr(outputs.get("root_entropy"))] + tail + \
-        [_stream(stream)]
+        outputs["root_entropy"] = _new_output(torch.empty, (logits.shape[0],), stream, dtype=torch.float32,
+                                              device=logits.device)
+    entropy = [_ptr(outputs["root_entropy"])] if want_entropy else []
+    args = head + [_ptr(outputs["argmax"])] + walk + entropy + tail + [_stream(stream)]
     return args, outputs, ws
 
 
@@ -347,7 +353,7 @@ def _sample_args(logits, parents, tokens, temperature, seed, round_, path_stride
         if round_counter.numel() != 1:
             raise ValueError("round_counter must hold one element")
     head, walk, tail, outputs, _ = _accept_common(logits, parents, tokens, path_stride, outputs, workspace,
-                                                  "draws")
+                                                  "draws", stream)
     args = head + [ctypes.c_float(float(temperature)), ctypes.c_uint64(seed), ctypes.c_uint32(round_),
                    _ptr(round_counter), _ptr(outputs["draws"])] + walk + tail + [_stream(stream)]
     return args, outputs
@@ -368,11 +374,10 @@ def _tree_args(draft_logits, roots, budget, first_row, horizon, outputs, workspa
     dev = draft_logits.device
     n = int(budget) + 1
     if outputs is None:
-        outputs = {
-            "parents": torch.empty((batch, n), dtype=torch.int32, device=dev),
-            "tokens": torch.empty((batch, n), dtype=torch.int32, device=dev),
-            "scores": torch.empty((batch, n), dtype=torch.float32, device=dev) if want_scores else None,
-        }
+        def new(dt):
+            return _new_output(torch.empty, (batch, n), stream, dtype=dt, device=dev)
+        outputs = {"parents": new(torch.int32), "tokens": new(torch.int32),
+                   "scores": new(torch.float32) if want_scores else None}
     for name, dt in (("parents", torch.int32), ("tokens", torch.int32), ("scores", torch.float32)):
         t = outputs.get(name)
         if t is not None:
@@ -382,7 +387,7 @@ def _tree_args(draft_logits, roots, budget, first_row, horizon, outputs, workspa
     need = glance_tree_workspace_size(batch, horizon, vocab, budget)
     if need == 0:
         raise GlanceError(GLANCE_ERR_INVALID_ARG, glance_last_error())
-    ws = _workspace(need, dev, workspace)
+    ws = _workspace(need, dev, workspace, stream)
     base = ctypes.c_void_p(draft_logits.data_ptr() + first_row * vocab * draft_logits.element_size())
     args = [ctypes.c_int32(batch), ctypes.c_int32(horizon), ctypes.c_int32(vocab), ctypes.c_int32(int(budget)),
             ctypes.c_int(code), base, ctypes.c_int64(rows * vocab), _ptr(roots), _ptr(outputs["parents"]),
@@ -498,9 +503,10 @@ def prepare_greedy_accept(logits, parents, tokens, path_stride=None, outputs=Non
     """Returns (call, outputs): call() re-runs the acceptance into the outputs dict."""
     args, outputs, ws = _accept_args(logits, parents, tokens, path_stride, outputs, workspace, stream,
                                      want_entropy)
-    _check(lib().glance_greedy_accept(*args))
+    fn = _accept_fn(want_entropy)
+    _check(fn(*args))
     keep = (logits, parents, tokens, outputs, ws)
-    return PreparedCall(lib().glance_greedy_accept, args, keep), outputs
+    return PreparedCall(fn, args, keep), outputs
 
 
 def prepare_build_tree(draft_logits, roots, budget, first_row=0, horizon=None, outputs=None, workspace=None,

@@ -201,7 +201,7 @@ glance_status attn_common(bool tree, const glance_attn_shape* s, const void* q, 
 struct AcceptPlan {
   int chunks, chunk_len;                // greedy acceptance (bandwidth-bound)
   int sample_chunks, sample_chunk_len;  // sampling walk (ALU-bound: more workgroups)
-  size_t part_bytes, bytes;
+  size_t part_bytes, bytes;  // chunk words, then the root row's entropy chunks
 };
 
 glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptPlan* out) {
@@ -377,12 +377,12 @@ glance_status accept_setup(int32_t batch, int32_t n_nodes, int32_t vocab, glance
   return ok();
 }
 
-glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
-                                   glance_dtype logits_dtype, const void* logits,
-                                   const int32_t* parents, const int32_t* tokens,
-                                   int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
-                                   int32_t path_stride, int32_t* next_root, float* root_entropy,
-                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+namespace {
+glance_status greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab, glance_dtype logits_dtype,
+                            const void* logits, const int32_t* parents, const int32_t* tokens,
+                            int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path, int32_t path_stride,
+                            int32_t* next_root, float* root_entropy, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
   AcceptPlan pl;
   glance::AcceptParams p;
   glance_status st = accept_setup(batch, n_nodes, vocab, logits_dtype, logits, parents, tokens, argmax_out,
@@ -398,6 +398,28 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
   take_events(&e0, &e1);
   return check_hip(glance::launch_accept(p, logits_dtype == GLANCE_BF16, stream, e0, e1),
                    "accept kernel launch");
+}
+}  // namespace
+
+glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                   glance_dtype logits_dtype, const void* logits,
+                                   const int32_t* parents, const int32_t* tokens,
+                                   int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
+                                   int32_t path_stride, int32_t* next_root,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return greedy_accept(batch, n_nodes, vocab, logits_dtype, logits, parents, tokens, argmax_out, accept_len,
+                       accept_path, path_stride, next_root, nullptr, workspace, workspace_bytes, stream);
+}
+
+glance_status glance_greedy_accept_entropy(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                           glance_dtype logits_dtype, const void* logits,
+                                           const int32_t* parents, const int32_t* tokens,
+                                           int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
+                                           int32_t path_stride, int32_t* next_root, float* root_entropy,
+                                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!root_entropy) return fail(GLANCE_ERR_INVALID_ARG, "root_entropy is NULL");
+  return greedy_accept(batch, n_nodes, vocab, logits_dtype, logits, parents, tokens, argmax_out, accept_len,
+                       accept_path, path_stride, next_root, root_entropy, workspace, workspace_bytes, stream);
 }
 
 glance_status glance_sample_accept(int32_t batch, int32_t n_nodes, int32_t vocab,
@@ -544,7 +566,7 @@ glance_status glance_commit_path(int32_t batch, int32_t n_nodes, int32_t n_kv_he
   return check_hip(glance::launch_commit(p, stream, e0, e1), "commit kernel launch");
 }
 
-size_t glance_attn_workspace_size(const glance_attn_shape* s, int32_t is_verify) {
+size_t glance_attn_workspace_size(const glance_attn_shape* s, int is_verify) {
   (void)is_verify;  // the draft and the verify of one shape share a plan
   Plan pl;
   if (make_plan(s, &pl) != GLANCE_OK) return 0;

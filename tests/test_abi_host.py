@@ -126,17 +126,24 @@ def test_accept_argument_checks(lib):
     assert G.glance_accept_workspace_size(0, 64, 10) == 0
     assert G.glance_accept_workspace_size(1, 65, 10) == 0
     st = lib.glance_greedy_accept(1, 65, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16, FAKE,
-                                  None, FAKE, 1 << 20, None)
+                                  FAKE, 1 << 20, None)
     assert st == G.GLANCE_ERR_UNSUPPORTED
     st = lib.glance_greedy_accept(1, 8, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, FAKE,
-                                  None, FAKE, 1 << 20, None)
+                                  FAKE, 1 << 20, None)
     assert st == G.GLANCE_ERR_INVALID_ARG and "path_stride" in G.glance_last_error()
     st = lib.glance_greedy_accept(1, 8, 100, G.GLANCE_BF16, FAKE, None, FAKE, FAKE, FAKE, FAKE, 8, FAKE,
-                                  None, FAKE, 1 << 20, None)
+                                  FAKE, 1 << 20, None)
     assert st == G.GLANCE_ERR_INVALID_ARG and "parents" in G.glance_last_error()
     st = lib.glance_greedy_accept(1, 8, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8, FAKE,
-                                  None, FAKE, 1, None)
+                                  FAKE, 1, None)
     assert st == G.GLANCE_ERR_WORKSPACE
+    # the entropy variant takes the same checks and needs its output pointer
+    st = lib.glance_greedy_accept_entropy(1, 8, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8, FAKE,
+                                          None, FAKE, 1 << 20, None)
+    assert st == G.GLANCE_ERR_INVALID_ARG and "root_entropy" in G.glance_last_error()
+    st = lib.glance_greedy_accept_entropy(1, 65, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16, FAKE,
+                                          FAKE, FAKE, 1 << 20, None)
+    assert st == G.GLANCE_ERR_UNSUPPORTED
 
 
 def _sample(lib, n=8, temperature=1.0, parents=FAKE, draws=FAKE, ws=FAKE, ws_bytes=1 << 20, dtype=G.GLANCE_BF16,
@@ -258,3 +265,62 @@ def test_validate_generated_trees(lib):
 def test_kernel_events_need_both_or_neither(lib):
     assert lib.glance_set_kernel_events(FAKE, None) == G.GLANCE_ERR_INVALID_ARG
     assert lib.glance_set_kernel_events(None, None) == G.GLANCE_OK
+
+
+# The C contract of the hot path's boundary: return type and parameter types,
+# in order, of each call, and the layout of the shape struct and the enums.
+BOUNDARY = {
+    "glance_block_draft_attn": ("glance_status", [
+        "const glance_attn_shape*", "const void*", "const void*", "const void*", "const void*", "const void*",
+        "const int32_t*", "void*", "float*", "void*", "size_t", "hipStream_t"]),
+    "glance_tree_verify_attn": ("glance_status", [
+        "const glance_attn_shape*", "const void*", "const void*", "const void*", "const void*", "const void*",
+        "const int32_t*", "const int32_t*", "void*", "float*", "void*", "size_t", "hipStream_t"]),
+    "glance_greedy_accept": ("glance_status", [
+        "int32_t", "int32_t", "int32_t", "glance_dtype", "const void*", "const int32_t*", "const int32_t*",
+        "int32_t*", "int32_t*", "int32_t*", "int32_t", "int32_t*", "void*", "size_t", "hipStream_t"]),
+    "glance_attn_workspace_size": ("size_t", ["const glance_attn_shape*", "int"]),
+    "glance_accept_workspace_size": ("size_t", ["int32_t", "int32_t", "int32_t"]),
+    "glance_validate_tree": ("glance_status", ["int32_t", "const int32_t*", "const int32_t*", "int32_t"]),
+    "glance_status_string": ("const char*", ["glance_status"]),
+    "glance_last_error": ("const char*", []),
+}
+
+
+def _prototypes():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    text = re.sub(r"\s+", " ", text)
+    protos = {}
+    for m in re.finditer(r"([A-Za-z_][A-Za-z_0-9 ]*?\*?) ?\b(glance_[a-z_0-9]+) ?\(([^()]*)\) ?;", text):
+        ret, name, params = m.group(1).strip(), m.group(2), m.group(3).strip()
+        types = []
+        if params and params != "void":
+            for prm in params.split(","):
+                prm = prm.strip().replace(" *", "*")
+                words = prm.replace("*", "* ").split()
+                # the last word is the parameter's name
+                types.append(" ".join(words[:-1]).replace("* ", "*").replace(" *", "*").strip())
+        protos[name] = (ret.replace(" *", "*"), types)
+    return protos
+
+
+@pytest.mark.parametrize("name", sorted(BOUNDARY))
+def test_boundary_prototype(name):
+    protos = _prototypes()
+    assert name in protos, f"{name} is not declared in glance.h"
+    assert protos[name] == BOUNDARY[name]
+
+
+def test_boundary_types():
+    text = re.sub(r"\s+", " ", re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S))
+    fields = re.search(r"typedef struct \{(.*?)\} glance_attn_shape;", text).group(1)
+    assert [f.split()[-1] for f in fields.split(";") if f.strip()] == [
+        "batch", "n_new", "n_q_heads", "n_kv_heads", "head_dim", "ctx_capacity", "sm_scale", "dtype"]
+    assert [f.split()[0] for f in fields.split(";") if f.strip()] == ["int32_t"] * 6 + ["float", "glance_dtype"]
+    assert ctypes.sizeof(G.AttnShape) == 32
+    assert (G.GLANCE_OK, G.GLANCE_ERR_INVALID_ARG, G.GLANCE_ERR_UNSUPPORTED, G.GLANCE_ERR_WORKSPACE,
+            G.GLANCE_ERR_HIP) == (0, -1, -2, -3, -4)
+    assert (G.GLANCE_F32, G.GLANCE_BF16) == (0, 1)
+    assert re.search(r"GLANCE_OK = 0, GLANCE_ERR_INVALID_ARG = -1, GLANCE_ERR_UNSUPPORTED = -2, "
+                     r"GLANCE_ERR_WORKSPACE = -3, GLANCE_ERR_HIP = -4 \} glance_status;", text)
+    assert re.search(r"typedef enum \{ GLANCE_F32 = 0, GLANCE_BF16 = 1 \} glance_dtype;", text)

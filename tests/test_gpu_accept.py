@@ -222,3 +222,23 @@ def test_root_entropy(dtype, case):
     plain = G.glance_greedy_accept(logits.cuda(), par.cuda(), tok.cuda())
     for k in ("argmax", "accept_len", "accept_path", "next_root"):
         assert torch.equal(plain[k], res[k])
+
+
+def test_one_workspace_across_calls_and_shapes():
+    """One workspace serves greedy and sampling calls of different shapes in
+    turn: nothing a call reads from it was left by an earlier call."""
+    shapes = [(4, 64, 152064), (1, 16, 1000), (6, 33, 50000), (4, 64, 152064)]
+    need = max(G.glance_accept_workspace_size(*s) for s in shapes)
+    ws = torch.full((need,), 0xA5, dtype=torch.uint8, device="cuda")  # stale bytes
+    for i, (batch, n, vocab) in enumerate(shapes):
+        w = C.custom_workload("verify_4k", batch=batch, n_tree=n, depth_cap=min(15, n - 1), vocab=vocab)
+        par, tok = C.tree_inputs(w, 20 + i)
+        logits = C.planted_logits(w, par, tok, 20 + i)
+        got = G.glance_greedy_accept(logits.cuda(), par.cuda(), tok.cuda(), path_stride=16, workspace=ws)
+        torch.cuda.synchronize()
+        assert_accept_equal({k: v.cpu().numpy() for k, v in got.items()}, logits, par, tok, path_stride=16)
+        smp = G.glance_sample_accept(logits.cuda(), par.cuda(), tok.cuda(), 1.0, 5, i, path_stride=16,
+                                     workspace=ws)
+        torch.cuda.synchronize()
+        assert int(smp["accept_len"].min()) >= 0
+        print(f"[workspace reuse] call {i}: batch {batch} n {n} vocab {vocab} ok", flush=True)

@@ -152,7 +152,7 @@ class Decoder:
         self.logits_buf = torch.zeros(1, n, VOCAB, device="cuda")
         self.acc = G.glance_greedy_accept(self.logits_buf, self.parents, self.tokens, path_stride=16,
                                           want_entropy=True)
-        self.acc_ws = torch.empty(G.glance_accept_workspace_size(1, n, VOCAB), dtype=torch.uint8, device="cuda")
+        self.acc_ws = torch.zeros(G.glance_accept_workspace_size(1, n, VOCAB), dtype=torch.uint8, device="cuda")
         if temperature is not None:  # the sampling walk writes draws in place of argmax rows
             self.acc = {"draws": torch.zeros(1, n, dtype=torch.int32, device="cuda"),
                         "accept_len": torch.zeros(1, dtype=torch.int32, device="cuda"),

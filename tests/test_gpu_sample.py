@@ -230,7 +230,7 @@ def test_device_round_counter_gives_fresh_noise_on_graph_replays():
     dl, dp, dt = logits.cuda(), par.cuda(), tok.cuda()
     base, seed = 100, 5
     counter = torch.zeros(1, dtype=torch.int32, device="cuda")
-    ws = torch.empty(G.glance_accept_workspace_size(2, 8, 3000), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(G.glance_accept_workspace_size(2, 8, 3000), dtype=torch.uint8, device="cuda")
     out = G.glance_sample_accept(dl, dp, dt, 1.0, seed, base, path_stride=16, workspace=ws, round_counter=counter)
     torch.cuda.synchronize()
     assert int(counter.item()) == 1
