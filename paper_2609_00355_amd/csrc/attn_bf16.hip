@@ -13,11 +13,12 @@
 // slots; so a ragged batch gets pieces of equal cost rather than equal key
 // ranges, and no slot is spent on a sequence's padding.
 //
-// Waves.  Waves 0 .. tiles-1 compute one 32-row tile each.  All 8 waves
-// stream K/V tiles from HBM straight into LDS (global_load_lds, 16 bytes per
-// lane, no register staging), each its share of every tile, through rings
-// of four K stages and four V stages; one LDS barrier per tile orders the
-// loads and the reads (the ring's rule is stated at ring_wait).
+// Waves.  Waves 0 .. tiles-1 compute one 32-row tile each.  The waves
+// without rows (one to four of them issue) stream K/V tiles from HBM straight
+// into LDS (global_load_lds, 16 bytes per lane, no register staging), each
+// its share of every tile, through rings of four K stages and four V stages;
+// one LDS barrier per tile orders the loads and the reads (the ring's rule
+// is stated at ring_wait).
 //
 // Per tile a computing wave runs, for its 32 rows and the tile's 64 keys,
 //   S^T[key][row] = K[key][:] . Q[row][:]           (v_mfma_f32_32x32x16_bf16, A = K, B = Q^T)
@@ -260,51 +261,71 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
   if (pc.index == 0 && g == 0 && rgi == 0 && threadIdx.x == 0)
     p.plan[b] = make_int2(pc.count, pc.first);  // for the merge pass
 
-  // =========================== K/V streaming (all waves) ===========================
+  // =========================== K/V streaming ===========================
+  // A DMA instruction holds its wave until the memory pipeline takes it,
+  // hundreds of cycles when HBM is busy.  With at most four computing waves,
+  // waves 4-7 (which have no rows) issue everything and the computing waves
+  // none; with five to seven, every wave issues an equal share (one or two
+  // waves without rows could not issue a whole tile's loads in the time the
+  // computing waves take for it).
   const char* kc = static_cast<const char*>(p.k_ctx);
   const char* vc = static_cast<const char*>(p.v_ctx);
   const char* kn = static_cast<const char*>(p.k_new);
   const char* vn = static_cast<const char*>(p.v_new);
-  constexpr int SH = NB / 8;  // load instructions per wave per K (or V) tile
-  // Load r of a tile fills LDS rows r RPL .. r RPL + RPL - 1; lane i writes
-  // row r RPL + i / CH, chunk slot i % CH, which holds the row's chunk
-  // slot ^ swz(row).  This wave's loads are r = wave + 8 i.  Lane offsets
-  // within a full context tile (row stride RB) are computed once.
-  unsigned full_off[SH];
+  // This wave's loads of a K (or V) tile: r = first + stride i, i < per_side.
+  constexpr int kMaxLoads = NB / 4;
+  int first, stride, per_side;
+  if (p.tiles_rg <= 4) {
+    first = wave - 4;
+    stride = 4;
+    per_side = wave >= 4 ? NB / 4 : 0;
+  } else {
+    first = wave;
+    stride = 8;
+    per_side = NB / 8;
+  }
+  // Load r (0 <= r < NB) of a tile fills LDS rows r RPL .. r RPL + RPL - 1;
+  // lane i writes row r RPL + i / CH, chunk slot i % CH, which holds the
+  // row's chunk slot ^ swz(row).  The lane's row and its byte offset within
+  // a full context tile (row stride RB) are computed once per load slot.
+  int lrow[kMaxLoads];
+  unsigned lchunk[kMaxLoads];
 #pragma unroll
-  for (int i = 0; i < SH; ++i) {
-    const int row = (wave + 8 * i) * RPL + lane / CH;
-    full_off[i] = (unsigned)(row * RB + (((lane % CH) ^ swz<D>(row)) * 16));
+  for (int i = 0; i < kMaxLoads; ++i) {
+    lrow[i] = (first + stride * i) * RPL + lane / CH;
+    lchunk[i] = (unsigned)(((lane % CH) ^ swz<D>(lrow[i])) * 16);
   }
   auto issue = [&](int t, bool v_side) __attribute__((always_inline)) {
     const char* gfull = v_side ? vc : kc;
-    const unsigned lds = (unsigned)(size_t)(v_side ? sV : sK) + (unsigned)(t % kStages) * TB;
+    const unsigned lds = (unsigned)(size_t)(v_side ? sV : sK) + (unsigned)(t % kStages) * TB + first * 1024;
     const int j = tb + t;
     if (j < ct && 64 * j + 64 <= ctx) {  // full context tile: SGPR base + fixed lane offsets
-      const size_t off = (((size_t)b * p.hkv + g) * p.cap + 64 * (size_t)j) * RB;
+      const char* base = gfull + (((size_t)b * p.hkv + g) * p.cap + 64 * (size_t)j) * RB;
 #pragma unroll
-      for (int i = 0; i < SH; ++i) dma16(gfull + off, full_off[i], lds + (wave + 8 * i) * 1024);
+      for (int i = 0; i < kMaxLoads; ++i)
+        if (i < per_side) dma16(base, (unsigned)(lrow[i] * RB) + lchunk[i], lds + stride * i * 1024);
       return;
     }
     // ragged context tile or the new keys: rows past the valid ones re-read
     // the last valid row (their scores are masked, so P = 0 and V is finite)
     const char* base;
-    unsigned stride;
+    unsigned rstride;
     int nvalid;
     if (j < ct) {
       base = gfull + (((size_t)b * p.hkv + g) * p.cap + 64 * (size_t)j) * RB;
-      stride = RB;
+      rstride = RB;
       nvalid = ctx - 64 * j;
     } else {
       base = (v_side ? vn : kn) + ((size_t)b * p.n * p.hkv + g) * RB;
-      stride = (unsigned)p.hkv * RB;
+      rstride = (unsigned)p.hkv * RB;
       nvalid = p.n;
     }
 #pragma unroll
-    for (int i = 0; i < SH; ++i) {
-      const int row = (wave + 8 * i) * RPL + lane / CH;
-      const int src = row < nvalid ? row : nvalid - 1;
-      dma16(base, (unsigned)src * stride + (unsigned)(((lane % CH) ^ swz<D>(row)) * 16), lds + (wave + 8 * i) * 1024);
+    for (int i = 0; i < kMaxLoads; ++i) {
+      if (i < per_side) {
+        const int src = lrow[i] < nvalid ? lrow[i] : nvalid - 1;
+        dma16(base, (unsigned)src * rstride + lchunk[i], lds + stride * i * 1024);
+      }
     }
   };
   // Ring rule.  Tile t is read by the computing waves' matrix phases: K(t) in
@@ -314,12 +335,17 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
   // into them (group t; the prologue issues groups -3, -2, -1: K(0), then
   // K(1) V(0), then K(2) V(1)).  Barrier t needs K(t) and V(t - 1), both of
   // group t - 3, so before it each wave waits until at most its groups t - 2
-  // and t - 1 are in flight (vmcnt counts this wave's loads, in issue order).
+  // and t - 1 are in flight (vmcnt counts this wave's loads, in issue order):
+  // 2 per_side loads a group, so 4 per_side.  Every wave issues its
+  // share of every group: a share left out leaves stale rows in the stage,
+  // which the computing waves then read as tile data.
   auto ring_issue = [&](int t) __attribute__((always_inline)) {
+    if (per_side == 0) return;
     if (t + 3 < n_tiles) issue(t + 3, false);
     if (t + 2 < n_tiles) issue(t + 2, true);
   };
   auto ring_prologue = [&]() __attribute__((always_inline)) {
+    if (per_side == 0) return;
     issue(0, false);                    // group -3: K(0)
     if (n_tiles > 1) issue(1, false);   // group -2: K(1), V(0)
     issue(0, true);
@@ -327,12 +353,15 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
     if (n_tiles > 1) issue(1, true);
   };
   auto ring_wait = [&](int t) __attribute__((always_inline)) {
-    if (t + 2 < n_tiles) wait_vmcnt<4 * SH>();
-    else wait_vmcnt<0>();
+    if (per_side == 0) return;
+    if (t + 2 >= n_tiles) wait_vmcnt<0>();
+    else if (per_side == NB / 4) wait_vmcnt<NB>();  // 4 per_side
+    else wait_vmcnt<NB / 2>();                      // per_side = NB / 8
   };
 
   if (wave >= p.tiles_rg) {
-    // a wave without rows: streams its share and keeps the barrier count
+    // a wave without rows: streams its share of the tiles and keeps the
+    // barrier count
     ring_prologue();
     for (int t = 0; t < n_tiles; ++t) {
       ring_wait(t);
@@ -547,23 +576,25 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
   // barrier between the phases of every other wave.
   //
   // Ring invariant: stage s = t % 4 of the ring holds K(t) from its issue
-  // after barrier t - 3 and V(t) from its issue after barrier t - 2.  K(t) is
-  // read in X_t only (between barriers t and t + 1), V(t) in X_{t+1} only
-  // (between barriers t + 1 and t + 2).  The issue after barrier t writes
-  // K(t + 3) and V(t + 2) over K(t - 1) and V(t - 2), whose last reads were
-  // in X_{t-1}, which every wave ended before it arrived at barrier t.
+  // right after barrier t - 3 and V(t) from its issue right after barrier
+  // t - 2.  K(t) is read in X_t only (between barriers t and t + 1), V(t) in
+  // X_{t+1} only (between barriers t + 1 and t + 2).  The issue right after
+  // barrier t writes K(t + 3) and V(t + 2) over K(t - 1) and V(t - 2), whose
+  // last reads were in X_{t-1}, which every computing wave ended before it
+  // arrived at barrier t; and every wave waited for its own share of K(t) and
+  // V(t - 1) before it arrived there.
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
   using YES = std::true_type;
   using NO = std::false_type;
-  lds_barrier();  // barrier 0 (its wait came with the query's): K(0) has landed, the ancestor words are written
+  lds_barrier();  // barrier 0: K(0) has landed, the ancestor words are written
   ring_issue(0);
   xphase(I0{}, YES{}, NO{});
   auto step = [&](int t, auto SK_) __attribute__((always_inline)) {
     yphase(t - 1);
-    ring_wait(t);   // this wave's own DMA of K(t) and V(t - 1) is complete
+    ring_wait(t);   // this wave's own share of K(t) and V(t - 1) is complete
     lds_barrier();  // barrier t: every wave's is, and X_{t-1} has ended everywhere
     ring_issue(t);
     xphase(SK_, YES{}, YES{});
