@@ -19,6 +19,8 @@
  *                            plus the bonus token that becomes the next root;
  *   glance_greedy_accept_entropy  the same, plus the entropy of each root row
  *                            (the predictor of Sec. 4's entropy law);
+ *   glance_greedy_accept_noalloc  the same, with no workspace argument and no
+ *                            allocation (a static per-GPU scratch buffer);
  *   glance_sample_accept     the same walk under sampling at temperature T:
  *                            each row's token is a Gumbel-max draw from
  *                            softmax(z / T) with counter-based noise;
@@ -191,6 +193,26 @@ glance_status glance_greedy_accept_entropy(int32_t batch, int32_t n_nodes, int32
                                            int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
                                            int32_t path_stride, int32_t* next_root, float* root_entropy,
                                            void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * glance_greedy_accept for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same argmax and walk with the same outputs, but no
+ * workspace argument.  The scratch (the chunk words of every row) lives in a
+ * static 1 MiB device buffer that the library holds on every GPU it runs on
+ * until the process ends; the call allocates nothing.  Shapes whose scratch
+ * exceeds 1 MiB are rejected with GLANCE_ERR_UNSUPPORTED before any HIP call
+ * (batch * n_nodes up to 32768 always fit).  All calls on one GPU share its
+ * buffer: calls that overlap on one GPU (different streams without ordering,
+ * or several host threads) race and must be serialised by the caller.
+ * The first call on a device looks up that device's buffer address (one HIP
+ * symbol query, no allocation).
+ */
+glance_status glance_greedy_accept_noalloc(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                           glance_dtype logits_dtype, const void* logits,
+                                           const int32_t* parents, const int32_t* tokens,
+                                           int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
+                                           int32_t path_stride, int32_t* next_root, hipStream_t stream);
 
 /*
  * Sampling acceptance at temperature T > 0 (the Limitations section: under

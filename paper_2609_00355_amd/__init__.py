@@ -60,6 +60,8 @@ _SIGS = {
                                             _P, _P, _SZ, _P]),
     "glance_greedy_accept_entropy": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P, _P,
                                                     _I32, _P, _P, _P, _SZ, _P]),
+    "glance_greedy_accept_noalloc": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, _P, _P, _P, _I32,
+                                                    _P, _P]),
     "glance_sample_accept": (ctypes.c_int, [_I32, _I32, _I32, ctypes.c_int, _P, _P, _P, ctypes.c_float,
                                             ctypes.c_uint64, ctypes.c_uint32, _P, _P, _P, _P, _I32, _P, _P,
                                             _SZ, _P]),

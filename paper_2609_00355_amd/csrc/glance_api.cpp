@@ -330,6 +330,11 @@ glance_status glance_tree_verify_attn(const glance_attn_shape* s, const void* q,
                      workspace_bytes, stream);
 }
 
+void bind_accept_workspace(glance::AcceptParams* p, const AcceptPlan& pl, void* workspace) {
+  p->part = static_cast<unsigned long long*>(workspace);
+  p->ent_part = reinterpret_cast<float4*>(static_cast<char*>(workspace) + pl.part_bytes);
+}
+
 // Host checks and parameters shared by the greedy and the sampling
 // acceptance; `rows_name` names the per-row output in error messages.
 glance_status accept_setup(int32_t batch, int32_t n_nodes, int32_t vocab, glance_dtype logits_dtype,
@@ -368,8 +373,7 @@ glance_status accept_setup(int32_t batch, int32_t n_nodes, int32_t vocab, glance
   p->accept_len = accept_len;
   p->accept_path = accept_path;
   p->next_root = next_root;
-  p->part = static_cast<unsigned long long*>(workspace);
-  p->ent_part = reinterpret_cast<float4*>(static_cast<char*>(workspace) + pl->part_bytes);
+  bind_accept_workspace(p, *pl, workspace);
   p->batch = batch;
   p->n_nodes = n_nodes;
   p->vocab = vocab;
@@ -409,6 +413,36 @@ glance_status glance_greedy_accept(int32_t batch, int32_t n_nodes, int32_t vocab
                                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
   return greedy_accept(batch, n_nodes, vocab, logits_dtype, logits, parents, tokens, argmax_out, accept_len,
                        accept_path, path_stride, next_root, nullptr, workspace, workspace_bytes, stream);
+}
+
+glance_status glance_greedy_accept_noalloc(int32_t batch, int32_t n_nodes, int32_t vocab,
+                                           glance_dtype logits_dtype, const void* logits,
+                                           const int32_t* parents, const int32_t* tokens,
+                                           int32_t* argmax_out, int32_t* accept_len, int32_t* accept_path,
+                                           int32_t path_stride, int32_t* next_root, hipStream_t stream) {
+  AcceptPlan pl;
+  glance_status st = accept_plan(batch, n_nodes, vocab, &pl);
+  if (st != GLANCE_OK) return st;
+  const size_t cap = glance::noalloc_scratch_bytes();
+  if (pl.bytes > cap)
+    return fail(GLANCE_ERR_UNSUPPORTED,
+                "batch %d x n_nodes %d x vocab %d needs %zu bytes of scratch; the static buffer holds %zu",
+                batch, n_nodes, vocab, pl.bytes, cap);
+  // every host check first, against an aligned placeholder of the right size
+  glance::AcceptParams p;
+  st = accept_setup(batch, n_nodes, vocab, logits_dtype, logits, parents, tokens, argmax_out, "argmax_out",
+                    accept_len, accept_path, path_stride, next_root, reinterpret_cast<void*>(uintptr_t(256)),
+                    pl.bytes, &pl, &p);
+  if (st != GLANCE_OK) return st;
+  void* ws = nullptr;
+  if ((st = check_hip(glance::noalloc_scratch(&ws), "scratch address lookup")) != GLANCE_OK) return st;
+  bind_accept_workspace(&p, pl, ws);
+  p.chunks = pl.chunks;
+  p.chunk_len = pl.chunk_len;
+  hipEvent_t e0, e1;
+  take_events(&e0, &e1);
+  return check_hip(glance::launch_accept(p, logits_dtype == GLANCE_BF16, stream, e0, e1),
+                   "accept kernel launch");
 }
 
 glance_status glance_greedy_accept_entropy(int32_t batch, int32_t n_nodes, int32_t vocab,

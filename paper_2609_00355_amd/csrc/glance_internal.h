@@ -134,4 +134,9 @@ hipError_t launch_sample(const AcceptParams& p, bool bf16, hipStream_t s, hipEve
 hipError_t launch_tree(const TreeParams& p, bool bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_commit(const CommitParams& p, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
+// The static per-GPU scratch of the allocation-free entry points: its size,
+// and the current device's copy (looked up once per device).
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(void** out);
+
 }  // namespace glance

@@ -324,3 +324,17 @@ def test_boundary_types():
     assert re.search(r"GLANCE_OK = 0, GLANCE_ERR_INVALID_ARG = -1, GLANCE_ERR_UNSUPPORTED = -2, "
                      r"GLANCE_ERR_WORKSPACE = -3, GLANCE_ERR_HIP = -4 \} glance_status;", text)
     assert re.search(r"typedef enum \{ GLANCE_F32 = 0, GLANCE_BF16 = 1 \} glance_dtype;", text)
+
+
+def test_noalloc_accept_host_checks(lib):
+    """The allocation-free acceptance rejects, before any HIP call, shapes whose
+    scratch would not fit its static buffer, and the usual bad arguments."""
+    st = lib.glance_greedy_accept_noalloc(4096, 64, 1000, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16,
+                                          FAKE, None)
+    assert st == G.GLANCE_ERR_UNSUPPORTED and "static buffer" in G.glance_last_error()
+    st = lib.glance_greedy_accept_noalloc(1, 8, 100, G.GLANCE_BF16, FAKE, None, FAKE, FAKE, FAKE, FAKE, 8, FAKE,
+                                          None)
+    assert st == G.GLANCE_ERR_INVALID_ARG and "parents" in G.glance_last_error()
+    st = lib.glance_greedy_accept_noalloc(1, 65, 100, G.GLANCE_BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8, FAKE,
+                                          None)
+    assert st == G.GLANCE_ERR_UNSUPPORTED
