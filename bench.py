@@ -3,20 +3,25 @@
 A step is one pass of the whole hot path over one batch of synthetic input:
 block-draft attention, then tree-verify attention, then greedy acceptance
 (vocabulary argmax of every verified row and the walk), back to back on one
-stream.  The workload is the grounded long-document configuration: batch 4,
-28 query / 4 KV heads, head_dim 128, bf16, 16384 context tokens per sequence
-(14336 image + 2048 text), a 16-row draft block and a 64-row tree, verified
-rows over a 152064-token vocabulary.
+stream, replayed from a HIP graph captured once per input set (--eager: the
+prepared C-ABI calls one by one).  The headline workload is the grounded
+long-document configuration: batch 4, 28 query / 4 KV heads, head_dim 128,
+bf16, 16384 context tokens per sequence (14336 image + 2048 text), a 16-row
+draft block and a 64-row tree, verified rows over a 152064-token vocabulary.
 
 Inputs are resident in HBM before timing starts.  Several copies of the input
 set rotate from step to step so that each step's context reads miss the
-256 MB last-level cache (a step reads about 350 MB).  The draft and the
-verify read separate caches (the draft head's and the target's).
+256 MB last-level cache ("cold"; a doc_16k step reads about 350 MB); the
+"warm" figure replays one set, so whatever fits stays cached.  The draft and
+the verify read separate caches (the draft head's and the target's).
 
-Prints one JSON line: whole-round latency (value, from the wall clock over the
-timed steps), achieved KV HBM bandwidth, a per-kernel breakdown from HIP
-events recorded on the library's stream, the roofline of the dominant kernel
-and the float64 oracle timed on the host cores.
+Prints one JSON line per configuration: first the smaller configurations
+(tiny fp32, the 2k draft, the 4k verify, the ragged serving mix), each with
+its own round latency, p10/p90 over the timed steps, warm and cold, and the
+float64 oracle timed on a bounded sample; the last line is the headline
+(doc_16k): whole-round latency (value, from the wall clock over the timed
+steps), per-kernel times from HIP events recorded on the library's stream,
+the roofline of the dominant kernel and the oracle's time.
 """
 
 import argparse
@@ -47,10 +52,14 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="doc_16k")
+    ap.add_argument("--workload", default="doc_16k", help="the headline workload (last line)")
+    ap.add_argument("--configs", default="tiny_fp32,draft_2k,verify_4k,ragged_mix",
+                    help="workloads timed before the headline, one line each ('' for none)")
+    ap.add_argument("--eager", action="store_true", help="launch the prepared calls one by one (no HIP graph)")
     ap.add_argument("--sets", type=int, default=4, help="input copies rotated across steps")
-    ap.add_argument("--graph", action="store_true", help="replay the round from a captured HIP graph")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the oracle timing")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the headline's oracle timing")
+    ap.add_argument("--cpu-seconds-config", type=float, default=4.0,
+                    help="budget of each smaller configuration's oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (reference for HBM byte counters)")
@@ -160,38 +169,62 @@ def summarise_traffic(fetch_dir, write_dir):
     print(json.dumps(out))
 
 
-def cpu_baseline(inputs, budget_s):
-    """The float64 oracle, as it stands, on a bounded sample of the same round."""
-    import numpy as np
-    from oracle import accept as OA
-    from oracle import attention as OT
+def host_info():
+    """Host cores and CPU model for the oracle timing."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count() or 1
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
-        cores = os.cpu_count() or 1
+        threads = nproc
+    return {"nproc": int(nproc), "cpu_model": model, "blas_threads": int(threads)}
+
+
+def cpu_baseline(inputs, budget_s):
+    """The float64 oracle, as it stands, on a bounded sample of the same round:
+    whole sequences (every step of the workload for one sequence) until the
+    budget is spent, scaled to the full batch."""
+    from oracle import accept as OA
+    from oracle import attention as OT
     w = inputs["workload"]
-    d, v = inputs["draft"], inputs["verify"]
-    rows_per_batch = []
+    info = host_info()
     t0 = time.perf_counter()
     done_b = 0
-    # one sequence of the batch at a time (draft + verify + accept of that sequence)
     for b in range(w.batch):
         sl = slice(b, b + 1)
-        OT.block_draft_attn(d["q"][sl], d["k_ctx"][sl], d["v_ctx"][sl], d["k_new"][sl], d["v_new"][sl],
-                            d["ctx_lens"][sl])
-        OT.tree_verify_attn(v["q"][sl], v["k_ctx"][sl], v["v_ctx"][sl], v["k_new"][sl], v["v_new"][sl],
-                            v["ctx_lens"][sl], inputs["parents"][sl])
-        OA.greedy_accept(inputs["logits"][sl], inputs["parents"][sl], inputs["tokens"][sl])
+        if "draft" in w.steps:
+            d = inputs["draft"]
+            OT.block_draft_attn(d["q"][sl], d["k_ctx"][sl], d["v_ctx"][sl], d["k_new"][sl], d["v_new"][sl],
+                                d["ctx_lens"][sl])
+        if "verify" in w.steps:
+            v = inputs["verify"]
+            OT.tree_verify_attn(v["q"][sl], v["k_ctx"][sl], v["v_ctx"][sl], v["k_new"][sl], v["v_new"][sl],
+                                v["ctx_lens"][sl], inputs["parents"][sl])
+        if "accept" in w.steps:
+            OA.greedy_accept(inputs["logits"][sl], inputs["parents"][sl], inputs["tokens"][sl])
         done_b += 1
         if time.perf_counter() - t0 > budget_s:
             break
     dt = time.perf_counter() - t0
-    per_round_us = dt / done_b * w.batch * 1e6
-    rows_per_batch.append(done_b)
-    return {"value": round(per_round_us, 1), "unit": "us per round", "cores": int(cores), "kind": "oracle",
-            "sample": f"{done_b} of {w.batch} sequences of one {w.name} round (draft + verify + accept, "
-                      f"numpy float64), scaled to the full round; {dt:.1f} s"}
+    # scaled by context tokens when the lengths differ (ragged batches)
+    ctx = [int(c) for c in inputs["ctx_lens"]]
+    frac = (sum(ctx[:done_b]) + done_b) / (sum(ctx) + w.batch)
+    per_round_us = dt / frac * 1e6
+    return {"value": round(per_round_us, 1), "unit": "us per round", "cores": info["blas_threads"],
+            "nproc": info["nproc"], "cpu_model": info["cpu_model"], "kind": "oracle",
+            "sample": f"{done_b} of {w.batch} sequences of one {w.name} round ({' + '.join(w.steps)}, numpy "
+                      f"float64), scaled to the whole round by context tokens; {dt:.1f} s"}
 
 
 def verify_sweep(args, w, G, C, torch, np, dev):
@@ -280,7 +313,7 @@ def measure_commit(args, w, s, G, torch, np, dev, stream, ctx):
     values of the verify pass appended to a cache with room for them), timed
     with HIP events around its kernel; the lengths are reset between calls
     outside the timed interval."""
-    vv = s["keep"][1]
+    vv = s["keep"]["verify"][0]
     k_new, v_new = vv["k_new"], vv["v_new"]
     a_out = s["a_out"]
     cap = int(max(ctx)) + w.n_tree
@@ -319,12 +352,12 @@ def measure_sample(args, w, sets, G, torch, np, stream):
         b.record(stream)
     outs = []
     for s in sets:
-        logits, par, tok = s["keep"][4], s["keep"][2], s["keep"][3]
+        logits, par, tok = s["keep"]["logits"], s["keep"]["par"], s["keep"]["tok"]
         outs.append(G.glance_sample_accept(logits, par, tok, 1.0, 2026, 0, path_stride=16, stream=stream))
     torch.cuda.synchronize()
     for i in range(args.warmup + args.steps):
         s = sets[i % len(sets)]
-        logits, par, tok = s["keep"][4], s["keep"][2], s["keep"][3]
+        logits, par, tok = s["keep"]["logits"], s["keep"]["par"], s["keep"]["tok"]
         if i >= args.warmup:
             G.glance_set_kernel_events(*evs[i - args.warmup])
         G.glance_sample_accept(logits, par, tok, 1.0, 2026, i + 1, path_stride=16,
@@ -343,6 +376,230 @@ def measure_sample(args, w, sets, G, torch, np, stream):
             "peak_tops": VALU_PEAK_TOPS, "frac": round(ops / us / 1e6 / VALU_PEAK_TOPS, 4),
             "traffic": load_traffic("sample", os.path.join(ROOT, "paper_2609_00355_amd", "csrc", "accept.hip")),
             "mean_accept_len": round(float(acc.mean()), 3)}
+
+
+HEADLINE_METRIC = "draft+verify round latency (\u00b5s) and achieved KV HBM GB/s at 16k ctx, 1 MI355X"
+
+
+def prepare_sets(w, n_sets, G, C, torch, dev):
+    """Device copies of one round's inputs and the prepared calls of the
+    workload's steps, n_sets times (all copies hold the same values)."""
+    inputs = C.round_inputs(w, seed=0)
+    sets = []
+    for _ in range(n_sets):
+        s = {"calls": {}, "keep": {}}
+        if "verify" in w.steps or "accept" in w.steps:
+            s["keep"]["par"] = inputs["parents"].to(dev)
+            s["keep"]["tok"] = inputs["tokens"].to(dev)
+        if "draft" in w.steps:
+            dd = {k: t.to(dev) for k, t in inputs["draft"].items()}
+            call, out, _ = G.prepare_block_draft_attn(dd["q"], dd["k_ctx"], dd["v_ctx"], dd["k_new"], dd["v_new"],
+                                                      dd["ctx_lens"])
+            s["calls"]["draft"], s["keep"]["draft"] = call, (dd, out)
+        if "verify" in w.steps:
+            vv = {k: t.to(dev) for k, t in inputs["verify"].items()}
+            call, out, _ = G.prepare_tree_verify_attn(vv["q"], vv["k_ctx"], vv["v_ctx"], vv["k_new"], vv["v_new"],
+                                                      vv["ctx_lens"], s["keep"]["par"])
+            s["calls"]["verify"], s["keep"]["verify"] = call, (vv, out)
+        if "accept" in w.steps:
+            logits = inputs["logits"].to(dev)
+            call, a_out = G.prepare_greedy_accept(logits, s["keep"]["par"], s["keep"]["tok"], path_stride=16)
+            s["calls"]["accept"], s["keep"]["logits"], s["a_out"] = call, logits, a_out
+        sets.append(s)
+    return inputs, sets
+
+
+def run_step(s):
+    for name in ("draft", "verify", "accept"):
+        if name in s["calls"]:
+            s["calls"][name]()
+
+
+def time_rounds(args, sets, stream, torch, np):
+    """Round latency: the wall clock over exactly args.steps steps (rotating
+    the input sets), then per-step HIP events for p10/p50/p90 (cold: rotating
+    sets; warm: one set)."""
+    graphs = None
+    if not args.eager:
+        graphs = []
+        for s in sets:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                run_step(s)
+            graphs.append(g)
+        torch.cuda.synchronize()
+
+    def run(i, rotate=True):
+        k = i % len(sets) if rotate else 0
+        if graphs:
+            graphs[k].replay()
+        else:
+            run_step(sets[k])
+
+    for i in range(args.warmup):
+        run(i)
+    torch.cuda.synchronize()
+    # ---- timed region: exactly K steps, synchronised on both sides
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        run(i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    def per_step(rotate):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for i, (a, b) in enumerate(evs):
+            a.record(stream)
+            run(i, rotate)
+            b.record(stream)
+        torch.cuda.synchronize()
+        us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+        return [round(float(np.percentile(us, q)), 2) for q in (10, 50, 90)]
+
+    cold = per_step(True)
+    warm = per_step(False)
+    return {"wall_us": wall / args.steps * 1e6, "wall_s": wall, "cold": cold, "warm": warm,
+            "launch": "HIP graph replay (one graph per input set)" if graphs else "eager (prepared C-ABI calls)"}
+
+
+def kernel_times(args, sets, stream, G, torch, np):
+    """Per step of the round: the main kernel alone (HIP events the library
+    records around it on its stream) and the whole call (events around the
+    call: attention + merge pass, argmax + walk), eager, rotating sets."""
+    names = [k for k in ("draft", "verify", "accept") if k in sets[0]["calls"]]
+    reps = max(args.steps, 10)
+    ev = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    kern = {k: [ev() for _ in range(reps)] for k in names}
+    call = {k: [ev() for _ in range(reps)] for k in names}
+    for pairs in list(kern.values()) + list(call.values()):
+        for a, b in pairs:  # torch creates the HIP events lazily, at first record
+            a.record(stream)
+            b.record(stream)
+    torch.cuda.synchronize()
+    for i in range(reps):
+        s = sets[i % len(sets)]
+        for k in names:
+            G.glance_set_kernel_events(*kern[k][i])
+            call[k][i][0].record(stream)
+            s["calls"][k]()
+            call[k][i][1].record(stream)
+    torch.cuda.synchronize()
+    med = lambda pairs: float(np.median([a.elapsed_time(b) * 1e3 for a, b in pairs]))
+    return {k: med(kern[k]) for k in names}, {k: med(call[k]) for k in names}
+
+
+def round_work(w, inputs):
+    """Algorithmic bytes and flops of each step of one round."""
+    ctx = inputs["ctx_lens"]
+    kvb = kv_bytes(w, ctx) if w.dtype == "bf16" else kv_bytes(w, ctx) * 2
+    esz = 2 if w.dtype == "bf16" else 4
+    work = {}
+    if "draft" in w.steps:
+        qo = w.batch * w.n_draft * (w.hq + w.hkv) * w.d * esz * 2
+        work["draft"] = {"bytes": kvb + qo, "flops": attn_flops(w, ctx, w.n_draft, w.batch * w.n_draft * w.n_draft)}
+    if "verify" in w.steps:
+        qo = w.batch * w.n_tree * (w.hq + w.hkv) * w.d * esz * 2
+        vis = tree_visible_pairs(inputs["parents"].numpy())
+        work["verify"] = {"bytes": kvb + qo, "flops": attn_flops(w, ctx, w.n_tree, vis)}
+    if "accept" in w.steps:
+        work["accept"] = {"bytes": w.batch * w.n_tree * w.vocab * esz, "flops": 0.0}
+    return work, kvb
+
+
+def per_kernel_report(w, work, k_us, c_us):
+    mfma_peak = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else None
+    out = {}
+    for k in k_us:
+        gbps = work[k]["bytes"] / k_us[k] / 1e3
+        rec = {"us": round(k_us[k], 2), "call_us": round(c_us[k], 2), "gbps": round(gbps, 1)}
+        if k == "accept":
+            rec.update(kernel="argmax_partial", bound="hbm", frac=round(gbps / HBM_PEAK_GBS, 3))
+        else:
+            tf = work[k]["flops"] / k_us[k] / 1e6
+            rec["tflops"] = round(tf, 1)
+            rec["kernel"] = f"attn_bf16<{w.d},{'true' if k == 'verify' else 'false'}>" if w.dtype == "bf16" \
+                else f"attn_f32<{w.d},{'true' if k == 'verify' else 'false'}>"
+            if k == "verify" and mfma_peak:
+                rec.update(bound="mfma", frac=round(tf / mfma_peak, 3))
+            else:
+                rec.update(bound="hbm", frac=round(gbps / HBM_PEAK_GBS, 3))
+        out[k] = rec
+    return out
+
+
+def describe(w, inputs):
+    import numpy as np
+    ctx = [int(c) for c in inputs["ctx_lens"]]
+    if w.ctx_range:
+        ctxs = f"ctx {min(ctx)}..{max(ctx)} (uniform {w.ctx_range[0]}..{w.ctx_range[1]}, mean {np.mean(ctx):.0f})"
+    else:
+        ctxs = f"ctx {w.ctx} ({w.image} image + {w.ctx - w.image} text) per sequence"
+    dt = "bf16" if w.dtype == "bf16" else "fp32"
+    parts = [f"{w.name}: batch {w.batch}, {w.hq}/{w.hkv} heads, head_dim {w.d}, {dt}, {ctxs}"]
+    if "draft" in w.steps:
+        parts.append(f"draft block {w.n_draft}")
+    if "verify" in w.steps or "accept" in w.steps:
+        parts.append(f"tree {w.n_tree} rows")
+    if "accept" in w.steps:
+        parts.append(f"vocab {w.vocab}")
+    return ", ".join(parts) + "; steps: " + " + ".join(w.steps)
+
+
+def measure_config(args, name, G, C, torch, np, dev, stream, headline):
+    w = C.WORKLOADS[name]
+    t_gen = time.perf_counter()
+    inputs, sets = prepare_sets(w, args.sets, G, C, torch, dev)
+    t_gen = time.perf_counter() - t_gen
+    torch.cuda.synchronize()
+    rt = time_rounds(args, sets, stream, torch, np)
+    k_us, c_us = kernel_times(args, sets, stream, G, torch, np)
+    work, kvb = round_work(w, inputs)
+    per_kernel = per_kernel_report(w, work, k_us, c_us)
+    us_round = rt["wall_us"]
+    res = {
+        "metric": HEADLINE_METRIC if headline else f"round latency (\u00b5s) of the {name} configuration, 1 MI355X",
+        "value": round(us_round, 2),
+        "unit": "us per round",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us_round / 1e3, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": describe(w, inputs), "global_batch": w.batch,
+                   "seq_len": int(max(int(c) for c in inputs["ctx_lens"])), "parallelism": "single GPU",
+                   "launch": rt["launch"], "input_sets_rotated": args.sets},
+        "round_us_p10_p50_p90": {"cold": rt["cold"], "warm": rt["warm"]},
+        "kernels": per_kernel,
+        "input_gen_s": round(t_gen, 1),
+    }
+    if "draft" in k_us or "verify" in k_us:
+        att = [k for k in ("draft", "verify") if k in k_us]
+        res["achieved_kv_gbps"] = round(len(att) * kvb / sum(k_us[k] for k in att) / 1e3, 1)
+        res["round_kv_gbps"] = round(len(att) * kvb / us_round / 1e3, 1)
+    return w, inputs, sets, res, k_us, work
+
+
+def roofline(w, k_us, work):
+    dom = max(k_us, key=lambda k: k_us[k])
+    if dom == "verify" and w.dtype == "bf16":
+        ach = work["verify"]["flops"] / k_us["verify"] / 1e6
+        roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        ach = work[dom]["bytes"] / k_us[dom] / 1e3
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    src = os.path.join(ROOT, "paper_2609_00355_amd", "csrc", "accept.hip" if dom == "accept" else "attn_bf16.hip")
+    roof["traffic"] = load_traffic(dom, src)
+    roof["kernel"] = {"draft": "attn_bf16<128, false>", "verify": "attn_bf16<128, true>",
+                      "accept": "argmax_partial<true, true>"}[dom]
+    roof["launch_us"] = round(k_us[dom], 2)
+    return roof
 
 
 def main():
@@ -369,52 +626,24 @@ def main():
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
 
-    w = C.WORKLOADS[args.workload]
     if args.verify_sweep:
-        verify_sweep(args, w, G, C, torch, np, dev)
+        verify_sweep(args, C.WORKLOADS[args.workload], G, C, torch, np, dev)
         return
-    t_gen = time.perf_counter()
-    inputs = C.round_inputs(w, seed=0)
-    t_gen = time.perf_counter() - t_gen
-    ctx = inputs["ctx_lens"]
-    stream = torch.cuda.current_stream()
 
-    # ---- device copies of the input set, outputs and prepared calls.  With
-    # --graph the calls are bound to a side stream that the capture runs on.
-    if args.graph:
-        stream = torch.cuda.Stream()
-        torch.cuda.set_stream(stream)
-    sets = []
-    for r in range(args.sets):
-        dd = {k: t.to(dev) for k, t in inputs["draft"].items()}
-        vv = {k: t.to(dev) for k, t in inputs["verify"].items()}
-        par = inputs["parents"].to(dev)
-        tok = inputs["tokens"].to(dev)
-        logits = inputs["logits"].to(dev)
-        d_call, d_out, _ = G.prepare_block_draft_attn(dd["q"], dd["k_ctx"], dd["v_ctx"], dd["k_new"],
-                                                      dd["v_new"], dd["ctx_lens"])
-        v_call, v_out, _ = G.prepare_tree_verify_attn(vv["q"], vv["k_ctx"], vv["v_ctx"], vv["k_new"],
-                                                      vv["v_new"], vv["ctx_lens"], par)
-        a_call, a_out = G.prepare_greedy_accept(logits, par, tok, path_stride=16)
-        sets.append({"draft": d_call, "verify": v_call, "accept": a_call, "a_out": a_out,
-                     "keep": (dd, vv, par, tok, logits, d_out, v_out)})
-    torch.cuda.synchronize()
+    # the prepared calls are bound to this stream; graphs are captured on it
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
 
-    def step(s):
-        s["draft"]()
-        s["verify"]()
-        s["accept"]()
+    for name in [c for c in args.configs.split(",") if c and c != args.workload]:
+        w, inputs, sets, res, _, _ = measure_config(args, name, G, C, torch, np, dev, stream, headline=False)
+        if not args.no_cpu_baseline:
+            res["cpu_baseline"] = cpu_baseline(inputs, args.cpu_seconds_config)
+        print(json.dumps(res), flush=True)
+        del sets, inputs
+        torch.cuda.empty_cache()
 
-    graphs = None
-    if args.graph:
-        graphs = []
-        for s in sets:
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g, stream=stream):
-                step(s)
-            graphs.append(g)
-        torch.cuda.synchronize()
-
+    w, inputs, sets, res, k_us, work = measure_config(args, args.workload, G, C, torch, np, dev, stream,
+                                                      headline=True)
     if args.calibrate_copy:  # reference kernel for the HBM byte counters
         src_c = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
         dst_c = torch.empty_like(src_c)
@@ -422,124 +651,17 @@ def main():
             torch.neg(src_c, out=dst_c)  # a plain streaming kernel: reads and writes COPY_BYTES
         torch.cuda.synchronize()
         del src_c, dst_c
-
-    for i in range(args.warmup):
-        if graphs:
-            graphs[i % len(graphs)].replay()
-        else:
-            step(sets[i % len(sets)])
-    torch.cuda.synchronize()
-
-    # ---- timed region: exactly K steps, synchronised on both sides
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        if graphs:
-            graphs[i % len(graphs)].replay()
-        else:
-            step(sets[i % len(sets)])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    us_round = wall / args.steps * 1e6
-
-    # ---- per-kernel durations: HIP events recorded by the library around each
-    # call's main kernel, on the same stream, over the same number of steps
-    names = ("draft", "verify", "accept")
-    evs = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(args.steps)] for k in names}
-    rounds = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
-    for pairs in list(evs.values()) + [rounds]:  # torch creates the HIP events lazily, at first record
-        for a, b in pairs:
-            a.record(stream)
-            b.record(stream)
-    torch.cuda.synchronize()
-    for i in range(args.steps):
-        s = sets[i % len(sets)]
-        rounds[i][0].record(stream)
-        for k in names:
-            G.glance_set_kernel_events(*evs[k][i])
-            s[k]()
-        rounds[i][1].record(stream)
-    torch.cuda.synchronize()
-    k_us = {k: float(np.mean([a.elapsed_time(b) for a, b in evs[k]]) * 1e3) for k in names}
-    round_gpu_us = float(np.mean([a.elapsed_time(b) for a, b in rounds]) * 1e3)
-
-    # ---- algorithmic work per launch
-    kvb = kv_bytes(w, ctx)
-    qo_draft = w.batch * w.n_draft * w.hq * w.d * 2 * 2 + w.batch * w.n_draft * w.hkv * w.d * 2 * 2
-    qo_verify = w.batch * w.n_tree * w.hq * w.d * 2 * 2 + w.batch * w.n_tree * w.hkv * w.d * 2 * 2
-    vis_tree = tree_visible_pairs(inputs["parents"].numpy())
-    f_draft = attn_flops(w, ctx, w.n_draft, w.batch * w.n_draft * w.n_draft)
-    f_verify = attn_flops(w, ctx, w.n_tree, vis_tree)
-    logit_bytes = w.batch * w.n_tree * w.vocab * 2
-    per_kernel = {
-        "draft": {"us": round(k_us["draft"], 2), "kernel": "attn_bf16<128,false>",
-                  "gbps": round((kvb + qo_draft) / k_us["draft"] / 1e3, 1),
-                  "tflops": round(f_draft / k_us["draft"] / 1e6, 1)},
-        "verify": {"us": round(k_us["verify"], 2), "kernel": "attn_bf16<128,true>",
-                   "gbps": round((kvb + qo_verify) / k_us["verify"] / 1e3, 1),
-                   "tflops": round(f_verify / k_us["verify"] / 1e6, 1)},
-        "accept": {"us": round(k_us["accept"], 2), "kernel": "argmax_partial<true,true>",
-                   "gbps": round(logit_bytes / k_us["accept"] / 1e3, 1)},
-    }
-    for k, bound in (("draft", "hbm"), ("verify", "mfma"), ("accept", "hbm")):
-        pk = per_kernel[k]
-        pk["bound"] = bound
-        pk["frac"] = round(pk["gbps"] / HBM_PEAK_GBS if bound == "hbm" else pk["tflops"] / MFMA_BF16_PEAK_TFLOPS, 3)
-
-    dom = max(names, key=lambda k: k_us[k])
-    src = os.path.join(ROOT, "paper_2609_00355_amd", "csrc",
-                       "accept.hip" if dom == "accept" else "attn_bf16.hip")
-    if dom == "verify":
-        roof = {"bound": "mfma", "achieved": round(f_verify / k_us["verify"] / 1e6, 1),
-                "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
-    elif dom == "draft":
-        roof = {"bound": "hbm", "achieved": round((kvb + qo_draft) / k_us["draft"] / 1e3, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": round(logit_bytes / k_us["accept"] / 1e3, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = load_traffic(dom, src)
-    roof["kernel"] = per_kernel[dom]["kernel"]
-
-    tree = None if args.no_tree else measure_tree_builder(args, w, G, C, torch, np, dev, stream)
-    commit = measure_commit(args, w, sets[0], G, torch, np, dev, stream, ctx)
-    sample = measure_sample(args, w, sets, G, torch, np, stream)
-
-    acc = sets[0]["a_out"]["accept_len"].cpu().numpy()
-    res = {
-        "metric": "draft+verify round latency (us) and achieved KV HBM GB/s at 16k ctx, 1 MI355X",
-        "value": round(us_round, 2),
-        "unit": "us per round",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(wall / args.steps * 1e3, 4),
-        "higher_is_better": False,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": f"{w.name}: batch {w.batch}, {w.hq}/{w.hkv} heads, head_dim {w.d}, bf16, "
-                               f"ctx {w.ctx} ({w.image} image + {w.ctx - w.image} text) per sequence, "
-                               f"draft block {w.n_draft}, tree {w.n_tree} rows, vocab {w.vocab}",
-                   "global_batch": w.batch, "seq_len": w.ctx, "parallelism": "single GPU",
-                   "launch": "graph replay" if graphs else "eager (prepared C-ABI calls)",
-                   "input_sets_rotated": args.sets},
-        "achieved_kv_gbps": round(2 * kvb / (k_us["draft"] + k_us["verify"]) / 1e3, 1),
-        "round_kv_gbps": round(2 * kvb / us_round / 1e3, 1),
-        "round_gpu_us_events": round(round_gpu_us, 2),
-        "kernels": per_kernel,
-        "roofline": roof,
-        "synthetic_tau": round(1.0 + float(acc.mean()), 3),
-        "input_gen_s": round(t_gen, 1),
-    }
-    if tree is not None:
-        res["tree_builder"] = tree
-    res["commit"] = commit
-    res["sample_accept"] = sample
+    res["roofline"] = roofline(w, k_us, work)
+    if not args.eager and w.steps == ("draft", "verify", "accept"):
+        eager_args = argparse.Namespace(**{**vars(args), "eager": True})
+        res["eager_round_us"] = round(time_rounds(eager_args, sets, stream, torch, np)["wall_us"], 2)
+    if w.steps == ("draft", "verify", "accept") and w.dtype == "bf16":
+        acc = sets[0]["a_out"]["accept_len"].cpu().numpy()
+        res["synthetic_tau"] = round(1.0 + float(acc.mean()), 3)
+        if not args.no_tree:
+            res["tree_builder"] = measure_tree_builder(args, w, G, C, torch, np, dev, stream)
+        res["commit"] = measure_commit(args, w, sets[0], G, torch, np, dev, stream, inputs["ctx_lens"])
+        res["sample_accept"] = measure_sample(args, w, sets, G, torch, np, stream)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(inputs, args.cpu_seconds)
     print(json.dumps(res), flush=True)

@@ -368,10 +368,11 @@ const char* glance_last_error(void);
 /*
  * Profiling hook.  When both events are non-NULL, the next attention, accept,
  * commit or tree-builder call on this thread records `start` on its stream
- * right before its main kernel (the attention and its merge pass, the
- * vocabulary argmax kernel, the commit kernel, or all passes of the tree
- * builder) and `stop` right after it, then forgets the pair.  Arguments are hipEvent_t handles created by
- * the caller.  Pass NULLs to clear.
+ * right before its main kernel (the attention kernel without its merge pass,
+ * the vocabulary argmax kernel without the walk, the commit kernel, or all
+ * passes of the tree builder) and `stop` right after it, then forgets the
+ * pair.  Arguments are hipEvent_t handles created by the caller.  Pass NULLs
+ * to clear.
  */
 glance_status glance_set_kernel_events(void* start_event, void* stop_event);
 
