@@ -331,14 +331,14 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
   // Ring rule.  Tile t is read by the computing waves' matrix phases: K(t) in
   // X_t, V(t) in X_{t+1} (see the schedule below); X_{t-1} ends before barrier
   // t in every wave.  So right after barrier t the stages of K(t - 1) and
-  // V(t - 2) are free, and each wave issues its share of K(t + 3) and V(t + 2)
-  // into them (group t; the prologue issues groups -3, -2, -1: K(0), then
-  // K(1) V(0), then K(2) V(1)).  Barrier t needs K(t) and V(t - 1), both of
-  // group t - 3, so before it each wave waits until at most its groups t - 2
-  // and t - 1 are in flight (vmcnt counts this wave's loads, in issue order):
-  // 2 per_side loads a group, so 4 per_side.  Every wave issues its
-  // share of every group: a share left out leaves stale rows in the stage,
-  // which the computing waves then read as tile data.
+  // V(t - 2) are free, and before barrier t + 1 each wave issues its share of
+  // K(t + 3) and V(t + 2) into them (group t; the prologue issues groups -3,
+  // -2, -1: K(0), then K(1) V(0), then K(2) V(1)).  Barrier t needs K(t) and
+  // V(t - 1), both of group t - 3, so before it each wave waits until at most
+  // its groups t - 2 and t - 1 are in flight (vmcnt counts this wave's loads,
+  // in issue order): 2 per_side loads a group, so 4 per_side.  Every wave
+  // issues its share of every group: a share left out leaves stale rows in
+  // the stage, which the computing waves then read as tile data.
   auto ring_issue = [&](int t) __attribute__((always_inline)) {
     if (per_side == 0) return;
     if (t + 3 < n_tiles) issue(t + 3, false);
@@ -532,8 +532,9 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
 
   // Matrix phase X: Q.K^T of tile t from stage SK into S (if QK_) and P.V of
   // tile t - 1 from stage SV (if PV_), one MFMA of each in turn, operands two
-  // ahead.
-  auto xphase = [&](auto SK_, auto QK_, auto PV_) __attribute__((always_inline)) {
+  // ahead.  With ti >= 0 the wave issues its share of ring group ti halfway
+  // through the phase.
+  auto xphase = [&](auto SK_, auto QK_, auto PV_, int ti) __attribute__((always_inline)) {
     constexpr int SK = decltype(SK_)::value, SV = (SK + kStages - 1) % kStages;
     constexpr bool DO_QK = decltype(QK_)::value, DO_PV = decltype(PV_)::value;
     constexpr int NK = 2 * KS, NV = 4 * DB, NS = NK > NV ? NK : NV;
@@ -560,6 +561,7 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
         O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vr[idx], __builtin_bit_cast(bf16x8, Pw[u >> 1][u & 1]),
                                                         O[db], 0, 0, 0);
       }
+      if (idx == NS / 2 && ti >= 0) ring_issue(ti);
       __builtin_amdgcn_sched_barrier(0);
     }
 #if GLANCE_XPRIO
@@ -582,7 +584,9 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
   // barrier t writes K(t + 3) and V(t + 2) over K(t - 1) and V(t - 2), whose
   // last reads were in X_{t-1}, which every computing wave ended before it
   // arrived at barrier t; and every wave waited for its own share of K(t) and
-  // V(t - 1) before it arrived there.
+  // V(t - 1) before it arrived there.  (Waves 4-6 issue group t halfway
+  // through X_t rather than right after barrier t: still between barriers t
+  // and t + 1, and X_t reads only K(t) and V(t - 1).)
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
@@ -591,13 +595,16 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
   using NO = std::false_type;
   lds_barrier();  // barrier 0: K(0) has landed, the ancestor words are written
   ring_issue(0);
-  xphase(I0{}, YES{}, NO{});
+  xphase(I0{}, YES{}, NO{}, -1);
   auto step = [&](int t, auto SK_) __attribute__((always_inline)) {
     yphase(t - 1);
     ring_wait(t);   // this wave's own share of K(t) and V(t - 1) is complete
     lds_barrier();  // barrier t: every wave's is, and X_{t-1} has ended everywhere
-    ring_issue(t);
-    xphase(SK_, YES{}, YES{});
+    // group t: waves 0-3 issue right away, waves 4-6 halfway through X_t, so
+    // that of the two computing waves sharing a SIMD one computes while the
+    // other waits for the memory pipeline to take its loads
+    if (wave < 4) ring_issue(t);
+    xphase(SK_, YES{}, YES{}, wave < 4 ? -1 : t);
   };
   int t = 1;
   while (t < n_tiles) {
@@ -612,10 +619,10 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
   }
   yphase(n_tiles - 1);
   switch (n_tiles & 3) {  // P.V of the last tile, stage (n_tiles - 1) % 4
-    case 1: xphase(I1{}, NO{}, YES{}); break;
-    case 2: xphase(I2{}, NO{}, YES{}); break;
-    case 3: xphase(I3{}, NO{}, YES{}); break;
-    default: xphase(I0{}, NO{}, YES{}); break;
+    case 1: xphase(I1{}, NO{}, YES{}, -1); break;
+    case 2: xphase(I2{}, NO{}, YES{}, -1); break;
+    case 3: xphase(I3{}, NO{}, YES{}, -1); break;
+    default: xphase(I0{}, NO{}, YES{}, -1); break;
   }
 
   l_run += __shfl_xor(l_run, 32);  // lanes l and l + 32 hold the same row
