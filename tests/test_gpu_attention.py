@@ -194,7 +194,7 @@ def test_explicit_scale():
     assert_close(out, lse, ref_out, ref_lse, "bf16", "explicit scale")
 
 
-# ------------------------------------------------------------- full workload sizes (sampled rows)
+# ------------------------------------------------------------- full workload sizes
 def _sampled_full(name, kind, seed=0):
     w = C.WORKLOADS[name]
     ctx = C.context_lengths(w, seed)
@@ -216,6 +216,27 @@ def test_doc_16k_full_size_sampled(kind):
     _sampled_full("doc_16k", kind)
 
 
+@pytest.mark.parametrize("seed", [0, 1])
 @pytest.mark.parametrize("kind", ["draft", "verify"])
-def test_ragged_mix_full_size_sampled(kind):
-    _sampled_full("ragged_mix", kind)
+def test_ragged_mix_full_size_sampled(kind, seed):
+    _sampled_full("ragged_mix", kind, seed)
+
+
+# Every row of the full doc_16k shapes (batch 4, 16384 context keys, 28/4
+# heads) against the oracle, with sharp scores (Q, K, V ~ N(0, 1): softmax
+# mass on a few keys, so a misplaced key or a wrong mask shows) and with
+# tree-dominant keys (each node's own key aligned with its queries, so the
+# ancestor mask decides most of the mass).  The launch configuration is the
+# one the benchmark times.
+@pytest.mark.parametrize("variant", ["sharp1", "tree_dominant"])
+@pytest.mark.parametrize("kind", ["draft", "verify"])
+def test_doc_16k_every_row(kind, variant):
+    w = C.WORKLOADS["doc_16k"]
+    ctx = C.context_lengths(w, 0)
+    n = w.n_draft if kind == "draft" else w.n_tree
+    inp = C.attention_inputs(w, kind, n, ctx, 3, variant, False, cap=w.cap)
+    par = C.tree_inputs(w, 3)[0] if kind == "verify" else None
+    out, lse = run_attention(kind, inp, par)
+    ref_out, ref_lse = oracle_attention(kind, inp, par)
+    print(f"[doc_16k every row] {kind} {variant}", flush=True)
+    assert_close(out, lse, ref_out, ref_lse, w.dtype, f"doc_16k {kind} {variant} every row")
