@@ -60,6 +60,20 @@ struct Plan {
   size_t total;
 };
 
+// A glance_dtype as the integer the caller stored: a C caller may store any
+// int in the field, and reading an out-of-range value as the C++ enum type
+// would be undefined, so the bits are copied out and compared as an int.
+int dtype_bits(const glance_dtype& d) {
+  int v;
+  memcpy(&v, &d, sizeof v);
+  return v;
+}
+
+bool dtype_ok(const glance_dtype& d) {
+  const int v = dtype_bits(d);
+  return v == GLANCE_F32 || v == GLANCE_BF16;
+}
+
 glance_status check_shape(const glance_attn_shape* s) {
   if (!s) return fail(GLANCE_ERR_INVALID_ARG, "shape is NULL");
   if (s->batch < 1) return fail(GLANCE_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", s->batch);
@@ -75,8 +89,7 @@ glance_status check_shape(const glance_attn_shape* s) {
   if (s->head_dim != 64 && s->head_dim != 128)
     return fail(GLANCE_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", s->head_dim);
   if (s->ctx_capacity < 0) return fail(GLANCE_ERR_INVALID_ARG, "ctx_capacity must be >= 0");
-  if (s->dtype != GLANCE_F32 && s->dtype != GLANCE_BF16)
-    return fail(GLANCE_ERR_UNSUPPORTED, "dtype must be GLANCE_F32 or GLANCE_BF16");
+  if (!dtype_ok(s->dtype)) return fail(GLANCE_ERR_UNSUPPORTED, "dtype must be GLANCE_F32 or GLANCE_BF16");
   if (!(s->sm_scale == s->sm_scale) || isinf(s->sm_scale))
     return fail(GLANCE_ERR_INVALID_ARG, "sm_scale must be finite");
   // index arithmetic in the kernels: element offsets fit in 64 bits, per-tensor
@@ -211,7 +224,7 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
     return fail(GLANCE_ERR_UNSUPPORTED, "n_nodes must be in 1..64 (got %d)", n_nodes);
   if (vocab < 1 || vocab > (1 << 30)) return fail(GLANCE_ERR_INVALID_ARG, "vocab must be in 1..2^30");
   const long long rows = (long long)batch * n_nodes;
-  if (rows * (long long)vocab > (1LL << 40)) return fail(GLANCE_ERR_UNSUPPORTED, "logits too large");
+  if (rows > (1LL << 40) / vocab) return fail(GLANCE_ERR_UNSUPPORTED, "logits too large");  // rows * vocab > 2^40
   // about 512 workgroups over the grid (two per CU), chunks of at least 8192 values
   const long long target = 512;
   long long chunks = (target + rows - 1) / rows;
@@ -345,8 +358,7 @@ glance_status accept_setup(int32_t batch, int32_t n_nodes, int32_t vocab, glance
                            size_t workspace_bytes, AcceptPlan* pl, glance::AcceptParams* p) {
   glance_status st = accept_plan(batch, n_nodes, vocab, pl);
   if (st != GLANCE_OK) return st;
-  if (logits_dtype != GLANCE_F32 && logits_dtype != GLANCE_BF16)
-    return fail(GLANCE_ERR_UNSUPPORTED, "logits dtype must be GLANCE_F32 or GLANCE_BF16");
+  if (!dtype_ok(logits_dtype)) return fail(GLANCE_ERR_UNSUPPORTED, "logits dtype must be GLANCE_F32 or GLANCE_BF16");
   if (path_stride < 1) return fail(GLANCE_ERR_INVALID_ARG, "path_stride must be >= 1");
   struct {
     const void* ptr;
@@ -496,7 +508,7 @@ glance_status glance_build_tree(int32_t batch, int32_t horizon, int32_t vocab, i
   TreePlan pl;
   glance_status st = tree_plan(batch, horizon, vocab, budget, &pl);
   if (st != GLANCE_OK) return st;
-  if (logits_dtype != GLANCE_F32 && logits_dtype != GLANCE_BF16)
+  if (!dtype_ok(logits_dtype))
     return fail(GLANCE_ERR_UNSUPPORTED, "draft logits dtype must be GLANCE_F32 or GLANCE_BF16");
   if (seq_stride < (int64_t)horizon * vocab)
     return fail(GLANCE_ERR_INVALID_ARG, "seq_stride (%lld) must be >= horizon * vocab (%lld)",
@@ -561,7 +573,7 @@ glance_status glance_commit_path(int32_t batch, int32_t n_nodes, int32_t n_kv_he
   if (head_dim < 1 || head_dim > 1024) return fail(GLANCE_ERR_UNSUPPORTED, "head_dim must be in 1..1024");
   if (ctx_capacity < 1) return fail(GLANCE_ERR_INVALID_ARG, "ctx_capacity must be >= 1");
   if (path_stride < 1) return fail(GLANCE_ERR_INVALID_ARG, "path_stride must be >= 1");
-  if (dtype != GLANCE_F32 && dtype != GLANCE_BF16)
+  if (!dtype_ok(dtype))
     return fail(GLANCE_ERR_UNSUPPORTED, "dtype must be GLANCE_F32 or GLANCE_BF16");
   // per-sequence copy index arithmetic stays in 32 bits
   if ((long long)64 * n_kv_heads * head_dim * 2 > 0x7fffffffLL)
