@@ -6,15 +6,21 @@ TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
   verified row (Algorithm 1, App. B).  Ties go to the lowest index, as numpy's
   argmax does (it returns the first maximum); a NaN counts as larger than every
   number and the first NaN wins, again numpy's rule.  +0 and -0 compare equal.
-* ``greedy_walk``  -- Algorithm 1's loop: start at the root, take the argmax
-  token of the current row, descend to the child carrying that token if the
-  tree has one, otherwise stop and return the token as the new root.  The
-  child is looked up by a linear scan over the nodes in index order, so if a
-  (malformed) tree has two siblings with the same token the lower index wins.
-* ``accepted_length_def1`` -- an independent evaluation of Def. 1 (Sec. 3.3):
-  A(T) = max{k >= 0 : Y_{1:j} in T for all j <= k}.  For every node it climbs to
-  the root and checks that every edge carries the argmax token of the parent
-  row; the answer is the deepest such node.
+* ``accepted_length_def1`` -- Def. 1 (Sec. 3.3) evaluated directly, the
+  oracle's definition of acceptance: A(T) = max{k >= 0 : Y_{1:j} in T for all
+  j <= k}, the depth of the deepest node whose every edge carries the argmax
+  token of its parent's row.  For every node it climbs to the root and checks
+  the edges.  In a tree of distinct strings (distinct tokens among siblings)
+  that node is unique; the accepted path is its root chain and the bonus
+  token is its own row's argmax.
+* ``greedy_walk``  -- the same acceptance reached by descending from the root
+  (the form Algorithm 1 takes), kept as a cross-check: from each node, the
+  child whose edge token equals the node's argmax, if there is one.  A
+  malformed tree may give two siblings one token; the descent then takes the
+  lower index (the reading the library documents), where Def. 1's deepest
+  node need not be unique, so ``greedy_accept`` uses the descent for such
+  trees (and for parents arrays that are no tree).  Only children after their parent count (every child in a tree), so
+  the descent ends within n steps whatever the parents array holds.
 
 * ``row_entropy``  -- H = -sum_w p(w) log p(w) of p = softmax(row), in nats: the
   target's next-token entropy, which the paper's entropy law (Sec. 4) reads at
@@ -38,12 +44,8 @@ def argmax_rows(logits):
     return np.argmax(x, axis=-1).astype(np.int64)
 
 
-def _children_in_order(parents, v):
-    return [c for c in range(len(parents)) if parents[c] == v]
-
-
 def greedy_walk(argmax_row, parents, tokens):
-    """Algorithm 1's walk over one packed tree.
+    """Acceptance by descent over one packed tree (cross-check of Def. 1).
 
     argmax_row [n]  target-greedy token of each node's row
     parents    [n]  parents[0] = -1
@@ -56,20 +58,15 @@ def greedy_walk(argmax_row, parents, tokens):
     parents = [int(p) for p in parents]
     tokens = [int(t) for t in tokens]
     argmax_row = [int(t) for t in argmax_row]
-    v = 0
     path = [0]
-    for _ in range(len(parents)):
-        t = argmax_row[v]
-        nxt = None
-        for c in _children_in_order(parents, v):
-            if tokens[c] == t:
-                nxt = c
-                break
-        if nxt is None:
-            return len(path) - 1, path, t
-        path.append(nxt)
-        v = nxt
-    raise ValueError("walk did not terminate: parents do not form a tree")
+    while True:
+        v = path[-1]
+        # children of v after v carrying v's argmax token, lowest index first
+        # (in a tree every child comes after its parent, so this is every child)
+        match = [c for c in range(v + 1, len(parents)) if parents[c] == v and tokens[c] == argmax_row[v]]
+        if not match:
+            return len(path) - 1, path, argmax_row[v]
+        path.append(match[0])
 
 
 def accepted_length_def1(argmax_row, parents, tokens):
@@ -98,8 +95,24 @@ def accepted_length_def1(argmax_row, parents, tokens):
     return best_depth, path
 
 
+def _tree_of_strings(parents, tokens):
+    """parents[0] = -1, every parent before its child, distinct tokens among
+    siblings: the packed tree is a set of distinct strings (Def. 1)."""
+    if int(parents[0]) != -1:
+        return False
+    seen = set()
+    for c in range(1, len(parents)):
+        key = (int(parents[c]), int(tokens[c]))
+        if not 0 <= key[0] < c or key in seen:
+            return False
+        seen.add(key)
+    return True
+
+
 def greedy_accept(logits, parents, tokens, path_stride=None):
-    """Batched acceptance: argmax of every row, then the walk of every sequence.
+    """Batched acceptance: argmax of every row, then each sequence's accepted
+    path by Def. 1 (by descent where the parents and tokens do not form a tree
+    of distinct strings).
 
     logits [batch][n][V]; parents, tokens [batch][n].
     Returns dict with argmax [batch][n], accept_len [batch], accept_path
@@ -117,7 +130,12 @@ def greedy_accept(logits, parents, tokens, path_stride=None):
     roots = np.zeros(batch, dtype=np.int64)
     committed = []
     for b in range(batch):
-        a, path, nr = greedy_walk(am[b], parents[b], tokens[b])
+        if _tree_of_strings(parents[b], tokens[b]):
+            a, path = accepted_length_def1(am[b], parents[b], tokens[b])
+            nr = int(am[b][path[-1]])
+            assert (a, path, nr) == greedy_walk(am[b], parents[b], tokens[b])
+        else:
+            a, path, nr = greedy_walk(am[b], parents[b], tokens[b])
         acc[b] = a
         k = min(len(path), path_stride)
         paths[b, :k] = path[:k]
