@@ -240,3 +240,26 @@ def test_doc_16k_every_row(kind, variant):
     ref_out, ref_lse = oracle_attention(kind, inp, par)
     print(f"[doc_16k every row] {kind} {variant}", flush=True)
     assert_close(out, lse, ref_out, ref_lse, w.dtype, f"doc_16k {kind} {variant} every row")
+
+
+def test_ragged_mix_plan_balance():
+    """The piece plan the kernels derive from the device context lengths
+    (read back from the workspace: pieces and first slot per sequence) gives
+    the ragged serving mix pieces whose longest is within 1.5x the mean keys
+    per piece, and covers every sequence's tiles."""
+    w = C.WORKLOADS["ragged_mix"]
+    ctx = C.context_lengths(w, 0)
+    inp = C.attention_inputs(w, "verify", w.n_tree, ctx, 0, None, False, cap=w.cap)
+    par, _ = C.tree_inputs(w, 0)
+    ws = torch.zeros(256 << 20, dtype=torch.uint8, device="cuda")
+    run_attention("verify", inp, par, workspace=ws)
+    plan = ws[: 8 * w.batch].cpu().view(torch.int32).numpy().reshape(w.batch, 2)  # (pieces, first slot)
+    tiles = np.array([(int(c) + 63) // 64 + 1 for c in ctx])  # context tiles + the new-key tile
+    count = plan[:, 0]
+    assert np.all(count >= 1)
+    # pieces of one sequence take consecutive slots, sequence after sequence
+    assert plan[0, 1] == 0 and np.all(plan[1:, 1] == plan[:-1, 1] + count[:-1])
+    longest = int(np.max((tiles + count - 1) // count))
+    mean = tiles.sum() / count.sum()
+    print(f"[ragged plan] pieces {count.tolist()} longest {longest} tiles, mean {mean:.1f}", flush=True)
+    assert longest <= 1.5 * mean
