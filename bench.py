@@ -193,15 +193,18 @@ def host_info():
 
 def cpu_baseline(inputs, budget_s):
     """The float64 oracle, as it stands, on a bounded sample of the same round:
-    whole sequences (every step of the workload for one sequence) until the
-    budget is spent, scaled to the full batch."""
+    whole sequences (every step of the workload for one sequence), round after
+    round, until the time budget is spent; the rate is scaled to one round by
+    context tokens."""
     from oracle import accept as OA
     from oracle import attention as OT
     w = inputs["workload"]
     info = host_info()
+    ctx = [int(c) for c in inputs["ctx_lens"]]
     t0 = time.perf_counter()
-    done_b = 0
-    for b in range(w.batch):
+    done, tok_done = 0, 0
+    while True:
+        b = done % w.batch
         sl = slice(b, b + 1)
         if "draft" in w.steps:
             d = inputs["draft"]
@@ -213,18 +216,16 @@ def cpu_baseline(inputs, budget_s):
                                 v["ctx_lens"][sl], inputs["parents"][sl])
         if "accept" in w.steps:
             OA.greedy_accept(inputs["logits"][sl], inputs["parents"][sl], inputs["tokens"][sl])
-        done_b += 1
+        done += 1
+        tok_done += ctx[b] + 1
         if time.perf_counter() - t0 > budget_s:
             break
     dt = time.perf_counter() - t0
-    # scaled by context tokens when the lengths differ (ragged batches)
-    ctx = [int(c) for c in inputs["ctx_lens"]]
-    frac = (sum(ctx[:done_b]) + done_b) / (sum(ctx) + w.batch)
-    per_round_us = dt / frac * 1e6
+    per_round_us = dt * (sum(ctx) + w.batch) / tok_done * 1e6
     return {"value": round(per_round_us, 1), "unit": "us per round", "cores": info["blas_threads"],
             "nproc": info["nproc"], "cpu_model": info["cpu_model"], "kind": "oracle",
-            "sample": f"{done_b} of {w.batch} sequences of one {w.name} round ({' + '.join(w.steps)}, numpy "
-                      f"float64), scaled to the whole round by context tokens; {dt:.1f} s"}
+            "sample": f"{done} sequence passes ({done / w.batch:.2f} rounds) of {w.name} ({' + '.join(w.steps)}, "
+                      f"numpy float64), scaled to one round by context tokens; {dt:.1f} s"}
 
 
 def verify_sweep(args, w, G, C, torch, np, dev):
