@@ -380,11 +380,13 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
   const int hl = row_ok ? row - node * p.group : 0;
   const size_t out_row = ((size_t)b * p.n + node) * p.hq + (size_t)g * p.group + hl;
 
-  // Query of the lane's row, dims 16 ks + 8 h .. +7: the B operands of
-  // Q.K^T, and (wave 0, tree) the parents.  Ordinary loads, made to land
-  // before this wave issues its first tile loads: the compiler counts only
-  // the loads it sees, so a wait it placed later would also wait for tile
-  // loads issued in between.
+  // This wave's share of the first three ring groups, then the query of the
+  // lane's row (dims 16 ks + 8 h .. +7: the B operands of Q.K^T) and (wave 0,
+  // tree) the parents, all in flight together.  The query and parents are
+  // ordinary loads issued after the tile loads: a wait the compiler places
+  // for them (it counts only the loads it sees) also covers the older tile
+  // loads, which completes more than it needs but never less.
+  ring_prologue();
   bf16x8 qf[KS];
   {
     const __bf16* qp = static_cast<const __bf16*>(p.q) + out_row * D + 8 * h;
@@ -394,10 +396,6 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
   const bool tree_words = TREE && has_new && wave == 0;
   int par = -1;
   if (tree_words && lane < p.n) par = p.parents[(size_t)b * p.n + lane];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) asm volatile("" ::"v"(qf[ks]));  // used here: the loads have landed
-  asm volatile("" ::"v"(par));
-  ring_prologue();
   ring_wait(0);
   // ancestor words of the packed tree, anc[i] = {i} u anc[parent(i)], by
   // pointer doubling in wave 0: after r rounds lane i holds its root path
