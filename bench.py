@@ -117,11 +117,11 @@ def load_traffic(kernel_key, src):
 COPY_BYTES = 256 << 20
 COPY_KERNEL = "neg_kernel"  # the calibration copy: out = -in over COPY_BYTES of fp32
 KERNEL_KEYS = {"draft": "attn_bf16<128, false", "verify": "attn_bf16<128, true",
-               "accept": "argmax_partial<true, true>", "tree_stats": "tree_stats<true>",
-               "tree_cands": "tree_cands<true>", "tree_rank": "tree_rank<true>", "tree_enum": "tree_enum",
+               "accept": "argmax_partial<true, true>", "tree_scan": "tree_scan<true>",
+               "tree_rank": "tree_rank<true>", "tree_enum": "tree_enum",
                "sample": "sample_partial<true, true>"}
 KERNEL_SRC = {"draft": "attn_bf16.hip", "verify": "attn_bf16.hip", "accept": "accept.hip",
-              "tree_stats": "tree.hip", "tree_cands": "tree.hip", "tree_rank": "tree.hip", "tree_enum": "tree.hip",
+              "tree_scan": "tree.hip", "tree_rank": "tree.hip", "tree_enum": "tree.hip",
               "sample": "accept.hip"}
 
 
@@ -301,9 +301,9 @@ def measure_tree_builder(args, w, G, C, torch, np, dev, stream):
             d[i] = d[par[b, i]] + 1
         depth.append(max(d))
     src = os.path.join(ROOT, "paper_2609_00355_amd", "csrc", "tree.hip")
-    parts = [load_traffic(k, src) for k in ("tree_stats", "tree_cands", "tree_rank", "tree_enum")]
+    parts = [load_traffic(k, src) for k in ("tree_scan", "tree_rank", "tree_enum")]
     traffic = sum(parts) if all(t is not None for t in parts) else None
-    return {"us": round(us, 2), "kernels": "tree_stats + tree_cands + tree_rank + tree_enum",
+    return {"us": round(us, 2), "kernels": "tree_scan + tree_rank + tree_enum",
             "input": f"drafter logits {w.batch} x {w.n_draft - 1} x {w.vocab} bf16, budget {budget}",
             "gbps": round(gbps, 1), "bound": "hbm", "frac": round(gbps / HBM_PEAK_GBS, 4),
             "traffic": traffic, "tree_depth": depth}

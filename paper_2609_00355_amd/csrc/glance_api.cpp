@@ -257,7 +257,7 @@ glance_status accept_plan(int32_t batch, int32_t n_nodes, int32_t vocab, AcceptP
 
 struct TreePlan {
   glance::TreeParams p;  // sizes and workspace offsets; pointers filled per call
-  size_t off_stats, off_sketch, off_cand, off_ccount, off_lq, off_tok, bytes;
+  size_t off_stats, off_sketch, off_thr, off_cand, off_ccount, off_lq, off_tok, bytes;
 };
 
 glance_status tree_plan(int32_t batch, int32_t horizon, int32_t vocab, int32_t budget, TreePlan* out) {
@@ -313,6 +313,7 @@ glance_status tree_plan(int32_t batch, int32_t horizon, int32_t vocab, int32_t b
   };
   pl.off_stats = take((size_t)rows * p.slices * sizeof(float2));
   pl.off_sketch = take((size_t)rows * p.slices * p.groups * sizeof(float));
+  pl.off_thr = take((size_t)rows * p.slices * sizeof(float));
   pl.off_cand = take((size_t)rows * p.slices * glance::kTreeSliceCap * sizeof(unsigned long long));
   pl.off_ccount = take((size_t)rows * p.slices * sizeof(int32_t));
   pl.off_lq = take((size_t)rows * 64 * sizeof(float));
@@ -543,6 +544,7 @@ glance_status glance_build_tree(int32_t batch, int32_t horizon, int32_t vocab, i
   p.scores = scores;
   p.stats = reinterpret_cast<float2*>(ws + pl.off_stats);
   p.sketch = reinterpret_cast<float*>(ws + pl.off_sketch);
+  p.thr = reinterpret_cast<float*>(ws + pl.off_thr);
   p.cand = reinterpret_cast<unsigned long long*>(ws + pl.off_cand);
   p.lq = reinterpret_cast<float*>(ws + pl.off_lq);
   p.tok = reinterpret_cast<int32_t*>(ws + pl.off_tok);

@@ -77,15 +77,16 @@ constexpr int kTreeMaxBudget = 63;
 constexpr int kTreeMaxHorizon = 15;
 constexpr int kTreeSlice = 1024;   // values per slice (one wave-wide load of 16 per lane)
 constexpr int kTreeSlicesPerWave = 2;
-constexpr int kTreeSliceCap = 32;  // candidate slots per slice before the exact fallback
+constexpr int kTreeSliceCap = 64;  // candidate slots per slice before it is re-read
 constexpr int kTreeCap = 2048;     // candidates per row ranked by counting
 
 // Layouts (row = sequence * L + offset - 1):
 //   logits  sequence b, offset j (1..L) at logits + b*seq_stride + (j-1)*vocab
 //   stats   [rows][slices] (max, sum exp(x - max)) of each 1024-value slice
 //   sketch  [rows][slices * groups] maxima of disjoint lane groups
+//   thr     [rows][slices] each slice's own candidate threshold
 //   cand    [rows][slices][kTreeSliceCap] packed (order key, ~index) of the
-//           slice's values >= threshold; ccount [rows][slices] their number
+//           slice's values >= thr; ccount [rows][slices] their number
 //   lq, tok [rows][64] the row's K best tokens in rank order and their log q
 struct TreeParams {
   const void* logits;
@@ -96,6 +97,7 @@ struct TreeParams {
   float* scores;
   float2* stats;
   float* sketch;
+  float* thr;
   unsigned long long* cand;
   float* lq;
   int32_t* tok;

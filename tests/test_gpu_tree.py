@@ -192,6 +192,29 @@ def test_tie_and_masked_rows(variant):
     check_batch(z, roots, 63, out)
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_clustered_slice_takes_the_exact_fallback(dtype):
+    """Twenty of the row's best values in one 1024-value slice, five in each of
+    its four 16-lane rows: the slice keeps only the values at or above the
+    smallest row maximum (16 of them), so four of the row's best are left out
+    and the ranking pass must see that and select exactly from the whole row."""
+    g = torch.Generator().manual_seed(11)
+    z = torch.randn(1, 3, 152064, generator=g)
+    vpl = 8 if dtype == torch.bfloat16 else 4         # values per 16-byte load
+    for r in range(4):
+        for i in range(5):
+            z[0, 0, r * 16 * vpl + i * vpl] = 20.0 - 0.125 * (5 * r + i)
+    z = z.to(dtype)
+    roots = torch.tensor([5], dtype=torch.int32)
+    out = run_tree(z, roots, 63)
+    clean = check_batch(z, roots, 63, out)
+    if dtype == torch.float32:
+        assert clean == [True]
+    # all twenty planted tokens of the first offset are one-token strings
+    one_tok = {int(t) for p_, t in zip(out["parents"][0, 1:], out["tokens"][0, 1:]) if p_ == 0}
+    assert {r * 16 * vpl + i * vpl for r in range(4) for i in range(5)} <= one_tok
+
+
 @pytest.mark.parametrize("vocab", [3000, 152064])
 def test_uniform_rows_take_the_exact_fallback(vocab):
     """All logits equal: every value reaches the candidate list, which overflows
