@@ -270,7 +270,7 @@ def measure_tree_builder(args, w, G, C, torch, np, dev, stream):
     """The tree builder (Algorithm 1, second step) on the drafter's logits of the
     same workload: 15 offsets x vocab per sequence, budget 63.  Timed on its own
     (it is not one of the round's attention / acceptance kernels): HIP events
-    around its four kernels, median over the steps, rotating input copies."""
+    around its three kernels, median over the steps, rotating input copies."""
     budget = w.n_tree - 1
     calls = []
     for r in range(args.sets):
