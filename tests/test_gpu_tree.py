@@ -238,6 +238,20 @@ def test_small_and_odd_shapes(vocab, horizon, budget, dtype):
     check_batch(z, roots, budget, out)
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_vocabulary_beyond_one_slice_per_thread(dtype):
+    """300001 tokens: 293 slices of 1024 values, more than the ranking pass's
+    256 threads, so its loops over slices take a second round (and the last
+    slice is ragged)."""
+    w = W.WORKLOADS["tiny_fp32"]
+    z = W.draft_logits(w, seed=7, batch=2, horizon=3, vocab=300001, dtype=dtype)
+    roots = W.draft_roots(w, seed=7, batch=2, vocab=300001)
+    out = run_tree(z, roots, 63)
+    cleans = check_batch(z, roots, 63, out)
+    if dtype == torch.float32:
+        assert all(cleans)
+
+
 def test_row_of_minus_inf():
     z = torch.randn(1, 5, 700, generator=torch.Generator().manual_seed(3))
     z[0, 2] = float("-inf")
