@@ -87,7 +87,9 @@ constexpr int kTreeCap = 2048;     // candidates per row ranked by counting
 //   thr     [rows][slices] each slice's own candidate threshold
 //   cand    [rows][slices][kTreeSliceCap] packed (order key, ~index) of the
 //           slice's values >= thr; ccount [rows][slices] their number
-//   lq, tok [rows][64] the row's K best tokens in rank order and their log q
+//   lq, tok [rows][64] the row's K best tokens in rank order: tok[r] the token
+//           of rank r, lq[r] the log q of rank r + 1 (-inf past the K-th),
+//           lq[63] the log q of rank 0
 struct TreeParams {
   const void* logits;
   long long seq_stride;
