@@ -252,6 +252,41 @@ def test_vocabulary_beyond_one_slice_per_thread(dtype):
         assert all(cleans)
 
 
+@pytest.mark.parametrize("case", range(24))
+def test_seeded_sweep(case):
+    """Random shapes and value patterns (seeded): vocabularies from 3 to 70000,
+    1 to 15 offsets, budgets 1 to 63, fp32 and bf16, Gaussian rows with some
+    best values clustered into one 1024-value slice (the re-read path), some
+    rows with coarse integer logits (ties), and some masked to -inf."""
+    rng = np.random.default_rng(1000 + case)
+    vocab = int(rng.choice([3, 17, 130, 1000, 4099, 20000, 70000]))
+    horizon = int(rng.integers(1, 16))
+    budget = int(rng.integers(1, 64))
+    total = sum(vocab ** l for l in range(1, horizon + 1))
+    budget = min(budget, total)
+    dtype = torch.bfloat16 if case % 2 else torch.float32
+    batch = int(rng.integers(1, 4))
+    z = rng.normal(size=(batch, horizon, vocab))
+    for b in range(batch):
+        for j in range(horizon):
+            kind = rng.integers(0, 4)
+            if kind == 1 and vocab >= 1024:      # clustered best values in one slice
+                s0 = 1024 * int(rng.integers(0, vocab // 1024))
+                idx = s0 + rng.choice(1024, size=min(40, 1024), replace=False)
+                z[b, j, idx] = 6.0 + rng.normal(size=idx.size)
+            elif kind == 2:                       # coarse grid: exact ties
+                z[b, j] = np.round(z[b, j] * 2) / 2
+            elif kind == 3 and vocab > 5:         # mostly masked
+                keep = rng.choice(vocab, size=max(1, vocab // 7), replace=False)
+                m = np.full(vocab, -np.inf)
+                m[keep] = z[b, j, keep]
+                z[b, j] = m
+    z = torch.from_numpy(z.astype(np.float32)).to(dtype)
+    roots = torch.from_numpy(rng.integers(0, vocab, size=batch).astype(np.int32))
+    out = run_tree(z, roots, budget)
+    check_batch(z, roots, budget, out)
+
+
 def test_row_of_minus_inf():
     z = torch.randn(1, 5, 700, generator=torch.Generator().manual_seed(3))
     z[0, 2] = float("-inf")
