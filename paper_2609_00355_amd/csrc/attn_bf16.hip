@@ -61,7 +61,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 #define GLANCE_AHEAD 2
 #endif
 #ifndef GLANCE_XPRIO
-#define GLANCE_XPRIO 0
+#define GLANCE_XPRIO 1  // raised wave priority during the matrix phase
 #endif
 constexpr int kOperandsAhead = GLANCE_AHEAD;  // LDS operand reads issued ahead of their MFMA
 
