@@ -303,7 +303,8 @@ glance_status tree_plan(int32_t batch, int32_t horizon, int32_t vocab, int32_t b
       p.tau_rank = 1;
     }
   }
-  p.wgs_per_row = (p.slices + 4 * glance::kTreeSlicesPerWave - 1) / (4 * glance::kTreeSlicesPerWave);
+  p.wgs_per_row = (p.slices + glance::kTreeScanWaves * glance::kTreeSlicesPerWave - 1) /
+                  (glance::kTreeScanWaves * glance::kTreeSlicesPerWave);
   TreePlan pl;
   size_t off = 0;
   auto take = [&](size_t bytes) {

@@ -76,7 +76,8 @@ struct AcceptParams {
 constexpr int kTreeMaxBudget = 63;
 constexpr int kTreeMaxHorizon = 15;
 constexpr int kTreeSlice = 1024;   // values per slice (one wave-wide load of 16 per lane)
-constexpr int kTreeSlicesPerWave = 2;
+constexpr int kTreeSlicesPerWave = 1;
+constexpr int kTreeScanWaves = 4;   // waves per tree_scan workgroup
 constexpr int kTreeSliceCap = 64;  // candidate slots per slice before it is re-read
 constexpr int kTreeCap = 2048;     // candidates per row ranked by counting
 
@@ -110,7 +111,7 @@ struct TreeParams {
   int groups;       // sketch entries per slice, a power of two in 1..64
   int tau_buckets;  // B: threshold buckets over the sketch
   int tau_rank;     // j in 1..4: the bucket entry of rank j bounds the threshold; B * j >= k
-  int wgs_per_row;  // ceil(slices / (4 * kTreeSlicesPerWave))
+  int wgs_per_row;  // ceil(slices / (kTreeScanWaves * kTreeSlicesPerWave))
   int vec;          // rows are 16-byte aligned: vector loads
 };
 
