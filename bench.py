@@ -100,16 +100,18 @@ def source_hash(path):
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def load_traffic(kernel_key, src):
-    """HBM bytes per launch measured with rocprofv3 counters, if taken on the current source."""
+def load_traffic(kernel_key, src, workload):
+    """HBM bytes per launch measured with rocprofv3 counters, if taken on the current source and
+    on this workload (the counter runs time one workload)."""
     p = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(p):
         return None
     try:
-        rec = json.load(open(p)).get(kernel_key)
+        allrec = json.load(open(p))
     except Exception:
         return None
-    if not rec or rec.get("source_sha") != source_hash(src):
+    rec = allrec.get(kernel_key)
+    if not rec or rec.get("source_sha") != source_hash(src) or allrec.get("workload", "doc_16k") != workload:
         return None
     return rec.get("bytes_per_launch")
 
@@ -125,7 +127,7 @@ KERNEL_SRC = {"draft": "attn_bf16.hip", "verify": "attn_bf16.hip", "accept": "ac
               "sample": "accept.hip"}
 
 
-def summarise_traffic(fetch_dir, write_dir):
+def summarise_traffic(fetch_dir, write_dir, workload):
     """Per-launch HBM bytes of the round's main kernels from rocprofv3 counter CSVs.
 
     FETCH_SIZE and WRITE_SIZE read KiB per dispatch; each is scaled by the
@@ -155,7 +157,8 @@ def summarise_traffic(fetch_dir, write_dir):
     if not f_copy or not w_copy:
         raise SystemExit("no copy-kernel reading in the counter runs (use --calibrate-copy)")
     f_scale, w_scale = COPY_BYTES / (f_copy * 1024), COPY_BYTES / (w_copy * 1024)
-    out = {"copy_bytes": COPY_BYTES, "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)}
+    out = {"workload": workload, "copy_bytes": COPY_BYTES, "fetch_scale": round(f_scale, 4),
+           "write_scale": round(w_scale, 4)}
     for name, key in KERNEL_KEYS.items():
         f, w = avg(fetch, key), avg(write, key)
         if f is None or w is None:
@@ -301,7 +304,7 @@ def measure_tree_builder(args, w, G, C, torch, np, dev, stream):
             d[i] = d[par[b, i]] + 1
         depth.append(max(d))
     src = os.path.join(ROOT, "paper_2609_00355_amd", "csrc", "tree.hip")
-    parts = [load_traffic(k, src) for k in ("tree_scan", "tree_rank", "tree_enum")]
+    parts = [load_traffic(k, src, w.name) for k in ("tree_scan", "tree_rank", "tree_enum")]
     traffic = sum(parts) if all(t is not None for t in parts) else None
     return {"us": round(us, 2), "kernels": "tree_scan + tree_rank + tree_enum",
             "input": f"drafter logits {w.batch} x {w.n_draft - 1} x {w.vocab} bf16, budget {budget}",
@@ -375,7 +378,8 @@ def measure_sample(args, w, sets, G, torch, np, stream):
             "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4), "bound": "alu",
             "alu_ops_per_token": SAMPLE_OPS_PER_TOKEN, "achieved_tops": round(ops / us / 1e6, 2),
             "peak_tops": VALU_PEAK_TOPS, "frac": round(ops / us / 1e6 / VALU_PEAK_TOPS, 4),
-            "traffic": load_traffic("sample", os.path.join(ROOT, "paper_2609_00355_amd", "csrc", "accept.hip")),
+            "traffic": load_traffic("sample", os.path.join(ROOT, "paper_2609_00355_amd", "csrc", "accept.hip"),
+                                    w.name),
             "mean_accept_len": round(float(acc.mean()), 3)}
 
 
@@ -588,7 +592,7 @@ def measure_config(args, name, G, C, torch, np, dev, stream, headline):
     return w, inputs, sets, res, k_us, c_us, work
 
 
-def roofline(w, k_us, c_us, work):
+def roofline(w, k_us, c_us, work, per_kernel):
     dom = max(k_us, key=lambda k: k_us[k])
     if dom == "verify" and w.dtype == "bf16":
         ach = work["verify"]["flops"] / k_us["verify"] / 1e6
@@ -599,10 +603,10 @@ def roofline(w, k_us, c_us, work):
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     # the dominant step as the whole call (attention + its merge pass)
     roof["frac_with_merge"] = round(roof["frac"] * k_us[dom] / c_us[dom], 4)
-    src = os.path.join(ROOT, "paper_2609_00355_amd", "csrc", "accept.hip" if dom == "accept" else "attn_bf16.hip")
-    roof["traffic"] = load_traffic(dom, src)
-    roof["kernel"] = {"draft": "attn_bf16<128, false>", "verify": "attn_bf16<128, true>",
-                      "accept": "argmax_partial<true, true>"}[dom]
+    src = os.path.join(ROOT, "paper_2609_00355_amd", "csrc",
+                       "accept.hip" if dom == "accept" else "attn_bf16.hip" if w.dtype == "bf16" else "attn_f32.hip")
+    roof["traffic"] = load_traffic(dom, src, w.name)
+    roof["kernel"] = per_kernel[dom]["kernel"]
     roof["launch_us"] = round(k_us[dom], 2)
     return roof
 
@@ -610,7 +614,7 @@ def roofline(w, k_us, c_us, work):
 def main():
     args = parse()
     if args.traffic_from:
-        summarise_traffic(*args.traffic_from)
+        summarise_traffic(*args.traffic_from, args.workload)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -640,7 +644,9 @@ def main():
     torch.cuda.set_stream(stream)
 
     for name in [c for c in args.configs.split(",") if c and c != args.workload]:
-        w, inputs, sets, res, _, _, _ = measure_config(args, name, G, C, torch, np, dev, stream, headline=False)
+        w, inputs, sets, res, k_us, c_us, work = measure_config(args, name, G, C, torch, np, dev, stream,
+                                                                headline=False)
+        res["roofline"] = roofline(w, k_us, c_us, work, res["kernels"])
         if not args.no_cpu_baseline:
             res["cpu_baseline"] = cpu_baseline(inputs, args.cpu_seconds_config)
         print(json.dumps(res), flush=True)
@@ -656,7 +662,7 @@ def main():
             torch.neg(src_c, out=dst_c)  # a plain streaming kernel: reads and writes COPY_BYTES
         torch.cuda.synchronize()
         del src_c, dst_c
-    res["roofline"] = roofline(w, k_us, c_us, work)
+    res["roofline"] = roofline(w, k_us, c_us, work, res["kernels"])
     if not args.eager and w.steps == ("draft", "verify", "accept"):
         eager_args = argparse.Namespace(**{**vars(args), "eager": True})
         res["eager_round_us"] = round(time_rounds(eager_args, sets, stream, torch, np)["wall_us"], 2)

@@ -38,6 +38,14 @@ def test_bench_line_fields():
     assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1 and cpu["sample"]
     for extra in ("tree_builder", "commit", "sample_accept"):
         assert d[extra]["us"] > 0, extra
+    # every line (the smaller configurations too) names its own dominant
+    # kernel; counter traffic is attached only to the workload it was taken on
+    traffic_wl = json.load(open(os.path.join(ROOT, "profiles", "traffic.json"))).get("workload")
+    for e in [json.loads(l) for l in r.stdout.splitlines() if l.startswith("{")]:
+        roof = e["roofline"]
+        assert roof["kernel"] in {k["kernel"] for k in e["kernels"].values()}, (e["config"]["workload"], roof)
+        if not e["config"]["workload"].startswith(str(traffic_wl) + ":"):
+            assert roof["traffic"] is None, e["config"]["workload"]
 
 
 def test_bench_refuses_more_than_one_gpu():
