@@ -14,11 +14,12 @@
 // the attention itself.
 //
 // attn_merge_pieces (bf16 attention): the partials are the pieces' MFMA
-// register tiles (lane l of a 32-row tile holds row l % 32 and, in float4 k,
-// dims 32 (k / 4) + 8 (k % 4) + 4 (l / 32) .. +3).  A thread owns one
-// (row, four dims) and reads that float4 of every piece of its sequence, in
+// register tiles in fp16, each row scaled by a power of two that the row's
+// (max, sum) pair carries (lane l of a 32-row tile holds row l % 32 and, in
+// quad k, dims 32 (k / 4) + 8 (k % 4) + 4 (l / 32) .. +3).  A thread owns one
+// (row, four dims) and reads that quad of every piece of its sequence, in
 // piece order, all loads of a chunk of 16 pieces issued before any is used;
-// consecutive threads read consecutive lanes, 1 KB per wave-wide load.
+// consecutive threads read consecutive lanes, 512 bytes per wave-wide load.
 // Sequences with one piece were written by the attention kernel and are
 // skipped.
 #include "glance_internal.h"
@@ -28,6 +29,7 @@ namespace {
 
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kMergeWaves = 2;
+typedef __attribute__((ext_vector_type(4))) _Float16 f16x4;
 
 template <int D, bool BF16>
 __global__ __launch_bounds__(64 * kMergeWaves) void attn_merge_kernel(AttnParams p) {
@@ -128,9 +130,9 @@ __global__ __launch_bounds__(256) void attn_merge_pieces(AttnParams p) {
   const int d0 = 32 * (k >> 2) + 8 * (k & 3) + 4 * h;
 
   const size_t ws0 = ((size_t)g * p.slots_per_g + pl.y) * p.row_groups + rgi;  // piece q: ws0 + q * row_groups
-  const size_t o_stride = (size_t)p.row_groups * p.tiles_rg * KQ * 64;          // float4s between pieces
+  const size_t o_stride = (size_t)p.row_groups * p.tiles_rg * KQ * 64;          // fp16 quads between pieces
   const size_t ml_stride = (size_t)p.row_groups * p.rows_rg;
-  const float4* po = reinterpret_cast<const float4*>(p.part_o) + (ws0 * p.tiles_rg + w) * KQ * 64 + k * 64 + lane;
+  const f16x4* po = reinterpret_cast<const f16x4*>(p.part_o) + (ws0 * p.tiles_rg + w) * KQ * 64 + k * 64 + lane;
   const float2* pm = p.part_ml + ws0 * p.rows_rg + 32 * w + r32;
 
   float M = -__builtin_inff(), lsum = 0.f;
@@ -138,11 +140,11 @@ __global__ __launch_bounds__(256) void attn_merge_pieces(AttnParams p) {
   for (int q0 = 0; q0 < pl.x; q0 += kChunk) {
     const int cnt = min(kChunk, pl.x - q0);
     float2 ml[kChunk];
-    float4 v[kChunk];
+    f16x4 v[kChunk];
 #pragma unroll
     for (int u = 0; u < kChunk; ++u) {
       ml[u] = u < cnt ? pm[(size_t)(q0 + u) * ml_stride] : make_float2(-__builtin_inff(), 0.f);
-      v[u] = u < cnt ? po[(size_t)(q0 + u) * o_stride] : make_float4(0.f, 0.f, 0.f, 0.f);
+      v[u] = u < cnt ? po[(size_t)(q0 + u) * o_stride] : f16x4{};
     }
     float mc = M;
 #pragma unroll
@@ -154,10 +156,10 @@ __global__ __launch_bounds__(256) void attn_merge_pieces(AttnParams p) {
     for (int u = 0; u < kChunk; ++u) {
       const float wu = u < cnt ? exp2f(ml[u].x - mc) : 0.f;
       lsum = fmaf(wu, ml[u].y, lsum);
-      acc.x = fmaf(wu, v[u].x, acc.x);
-      acc.y = fmaf(wu, v[u].y, acc.y);
-      acc.z = fmaf(wu, v[u].z, acc.z);
-      acc.w = fmaf(wu, v[u].w, acc.w);
+      acc.x = fmaf(wu, (float)v[u][0], acc.x);
+      acc.y = fmaf(wu, (float)v[u][1], acc.y);
+      acc.z = fmaf(wu, (float)v[u][2], acc.z);
+      acc.w = fmaf(wu, (float)v[u][3], acc.w);
     }
     M = mc;
   }

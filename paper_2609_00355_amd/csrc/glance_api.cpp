@@ -128,7 +128,7 @@ glance_status make_plan(const glance_attn_shape* s, Plan* out) {
     const size_t wslots = (size_t)p.slots_per_g * p.hkv * p.row_groups;
     pl.counter_bytes = round_up((size_t)p.batch * sizeof(int2), 256);
     pl.part_ml_bytes = round_up(wslots * p.rows_rg * sizeof(float2), 256);
-    pl.part_o_bytes = round_up(wslots * p.rows_rg * p.d * sizeof(float), 256);
+    pl.part_o_bytes = round_up(wslots * p.rows_rg * p.d * sizeof(uint16_t), 256);  // fp16
   } else {
     p.row_groups = (p.rows + glance::kF32RowBlock - 1) / glance::kF32RowBlock;
     p.rows_pad = p.row_groups * glance::kF32RowBlock;
