@@ -118,7 +118,7 @@ def test_workspace_size_depends_on_the_shape_only(lib):
     assert out.stdout.split() == [str(a), str(G.glance_accept_workspace_size(4, 64, 152064))]
     # more sequences than piece slots: one slot per sequence
     big = G.glance_attn_workspace_size(_shape(batch=100, n_new=64, ctx_capacity=128), 1)
-    assert big >= 100 * 4 * 2 * 224 * 128 * 4
+    assert big >= 100 * 4 * 2 * 224 * (128 * 2 + 8)
 
 
 def test_accept_argument_checks(lib):
