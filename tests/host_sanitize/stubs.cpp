@@ -32,11 +32,11 @@ hipError_t launch_attn_bf16(const AttnParams& p, bool tree, hipStream_t, hipEven
   g_stub.ev0 = ev0;
   g_stub.ev1 = ev1;
   // the kernels' largest indices: plan[b], part_ml[ws rows_rg + row],
-  // part_o[(ws tiles_rg + wave) (D / 8) 64 + lane + ...] float4s
+  // part_o[(ws tiles_rg + wave) (D / 8) 64 + lane + ...] fp16 quads (8 bytes)
   const size_t wslots = (size_t)p.slots_per_g * p.hkv * p.row_groups;
   in_ws(p.plan, (size_t)p.batch * sizeof(int2), "piece table");
   in_ws(p.part_ml, wslots * p.rows_rg * sizeof(float2), "(max, sum) partials");
-  in_ws(p.part_o, wslots * p.tiles_rg * (size_t)(p.d / 8) * 64 * 16, "output partials");
+  in_ws(p.part_o, wslots * p.tiles_rg * (size_t)(p.d / 8) * 64 * 8, "output partials");
   if (p.tiles_rg < 1 || p.tiles_rg > 7 || p.rows_rg != 32 * p.tiles_rg) abort();
   if ((long long)p.row_groups * p.rows_rg < p.rows) abort();
   if (p.slots_per_g < p.batch) abort();
