@@ -630,25 +630,26 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
 
   if (split) {
     // Partial of this piece in fp16, in the MFMA layout (four values per lane
-    // per store, 512 bytes per wave-wide store).  The row is scaled by 2^-e,
-    // 2^e the smallest power of two above its largest |O|: every element lies
-    // in (-1, 1) and keeps 11 bits relative to the row's largest, whatever the
-    // range of V.  The row's (max * c, sum) become (max * c + e, sum 2^-e), so
-    // 2^(max * c) sum and O keep their ratio: the merge's weights and the
-    // log-sum-exp are those of the unscaled partial, and the scaling by a
-    // power of two rounds nothing.
+    // per store, 512 bytes per wave-wide store): the row's O / sum, scaled by
+    // 2^-e, 2^e the smallest power of two above its largest |O| / sum, so
+    // every stored value lies in (-1, 1) and keeps 11 bits relative to the
+    // row's largest, whatever the range of V.  The row's pair becomes
+    // (max * c + log2 sum + e, 2^-e): 2^(max * c) sum and O / sum are kept,
+    // so the merge's weights and the log-sum-exp are those of the unscaled
+    // partial.  O / sum is a convex combination of V rows, so 2^e stays
+    // within fp32; e >= -100 keeps 2^-e, and the merge's sum of up to a few
+    // hundred of them, finite.  A row with no visible key keeps (-inf, 0).
     float amax = 0.f;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(O[db][i]));
     amax = fmaxf(amax, __shfl_xor(amax, 32));  // lanes l and l + 32 hold the same row
-    // amax = f 2^e, f in [0.5, 1); e >= -64 keeps sum 2^-e finite (rows whose
-    // |O| all lie below 2^-64 keep them below 1, where fp16 flushes nothing
-    // that matters), and e <= 128 leaves sum 2^-e at least 2^-128 sum, a
-    // subnormal of 21 or more bits
-    const int e = amax > 0.f ? max(__builtin_amdgcn_frexp_expf(amax), -64) : 0;
-    const float sc = __builtin_amdgcn_ldexpf(1.f, -e);
+    const float linv = lsum > 0.f ? 1.f / lsum : 0.f;
+    const float rmax = amax * linv;
+    const int e = rmax > 0.f ? max(__builtin_amdgcn_frexp_expf(rmax), -100) : 0;  // rmax = f 2^e, f in [0.5, 1)
+    const float p2 = __builtin_amdgcn_ldexpf(1.f, -e);
+    const float sc = linv * p2;
     const size_t ws = ((size_t)g * p.slots_per_g + pc.first + pc.index) * p.row_groups + rgi;
     f16x4* po = reinterpret_cast<f16x4*>(p.part_o) + (ws * p.tiles_rg + wave) * (OV / 4) * 64 + lane;
 #pragma unroll
@@ -657,7 +658,9 @@ __global__ __launch_bounds__(512) void attn_bf16(AttnParams p) {
       for (int j = 0; j < 4; ++j)
         po[(db * 4 + j) * 64] = f16x4{(_Float16)(O[db][4 * j] * sc), (_Float16)(O[db][4 * j + 1] * sc),
                                       (_Float16)(O[db][4 * j + 2] * sc), (_Float16)(O[db][4 * j + 3] * sc)};
-    if (h == 0) p.part_ml[ws * p.rows_rg + 32 * wave + r32] = make_float2(M + (float)e, lsum * sc);
+    if (h == 0)
+      p.part_ml[ws * p.rows_rg + 32 * wave + r32] =
+          lsum > 0.f ? make_float2(M + __builtin_amdgcn_logf(lsum) + (float)e, p2) : make_float2(M, 0.f);
     return;
   }
 

@@ -19,9 +19,9 @@ constexpr int kF32RowBlock = kWaves * kF32RowsPerWave;
 //   k_new  [batch][n][hkv][d]        parents [batch][n]
 //   part_o  fp32 kernel: [batch][hkv][nsplit][rows_pad][d] f32 (unnormalised partial output)
 //           bf16 kernel: [slot * row_groups + rg][tiles_rg][d / 8][64 lanes] f16x4 (MFMA layout;
-//           each row scaled by 2^-e, e carried in part_ml)
+//           each row's O / sum scaled by 2^-e)
 //   part_ml fp32 kernel: [batch][hkv][nsplit][rows_pad] f32x2 (running max * scale*log2e, sum)
-//           bf16 kernel: [slot * row_groups + rg][rows_rg] f32x2 (max * scale*log2e + e, sum * 2^-e)
+//           bf16 kernel: [slot * row_groups + rg][rows_rg] f32x2 (max * scale*log2e + log2 sum + e, 2^-e)
 //   out    [batch][n][hq][d]         lse [batch][n][hq]
 // Row r of a (sequence, KV head) problem is new row r / group of query head
 // g * group + r % group.
