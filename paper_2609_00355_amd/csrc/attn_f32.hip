@@ -114,22 +114,8 @@ __global__ __launch_bounds__(kWaves * 64) void attn_f32_partial(AttnParams p) {
       qv[i] = reinterpret_cast<const float4*>(q + (((size_t)b * p.n + node) * p.hq + (size_t)g * p.group + hl) * D)[e - lrow * D4];
     }
   }
-  if (TREE && has_new && tid < p.n) sPar[tid] = p.parents[(size_t)b * p.n + tid];
-#pragma unroll
-  for (int i = 0; i < QPER; ++i) reinterpret_cast<float4*>(sQ)[tid + i * kWaves * 64] = qv[i];
-  __syncthreads();
-  // ancestor-or-self word of each tree node, walked in LDS
-  if (TREE && has_new && tid < p.n) {
-    unsigned long long a = 1ull << tid;
-    int cur = tid;
-    int c = sPar[tid];
-    for (int step = 0; step < 64 && c >= 0 && c < cur; ++step) {
-      a |= 1ull << c;
-      cur = c;
-      c = sPar[c];
-    }
-    sAnc[tid] = a;
-  }
+  int par = -1;
+  if (TREE && has_new && tid < p.n) par = p.parents[(size_t)b * p.n + tid];
 
   float o[RPW][DPL], m_run[RPW], l_run[RPW];
 #pragma unroll
@@ -178,8 +164,26 @@ __global__ __launch_bounds__(kWaves * 64) void attn_f32_partial(AttnParams p) {
       }
     }
   };
+  // The first tile's loads go out with the query's and the parents', so that
+  // one memory round trip brings all three.
   int nv_next = 0;
   if (n_tiles > 0) load_tile(0, nv_next);
+  if (TREE && has_new && tid < p.n) sPar[tid] = par;
+#pragma unroll
+  for (int i = 0; i < QPER; ++i) reinterpret_cast<float4*>(sQ)[tid + i * kWaves * 64] = qv[i];
+  __syncthreads();
+  // ancestor-or-self word of each tree node, walked in LDS
+  if (TREE && has_new && tid < p.n) {
+    unsigned long long a = 1ull << tid;
+    int cur = tid;
+    int c = sPar[tid];
+    for (int step = 0; step < 64 && c >= 0 && c < cur; ++step) {
+      a |= 1ull << c;
+      cur = c;
+      c = sPar[c];
+    }
+    sAnc[tid] = a;
+  }
   for (int t = 0; t < n_tiles; ++t) {
     const bool is_new = (t == n_ctx_tiles);
     const int nvalid = nv_next;
