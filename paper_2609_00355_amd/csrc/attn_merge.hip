@@ -108,8 +108,8 @@ __global__ __launch_bounds__(64 * kMergeWaves) void attn_merge_kernel(AttnParams
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_pieces(AttnParams p) {
-  constexpr int KQ = D / 8;    // float4s per lane of a tile (OV / 4)
-  constexpr int WG_K = 4;      // float4 slots per workgroup (one per wave)
+  constexpr int KQ = D / 8;    // quads of values per lane of a tile (OV / 4)
+  constexpr int WG_K = 4;      // quad slots per workgroup (one per wave)
   constexpr int kChunk = 16;
   const int lane = threadIdx.x & 63;
   const int k = (blockIdx.x % (KQ / WG_K)) * WG_K + (threadIdx.x >> 6);
